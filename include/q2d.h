@@ -1,0 +1,198 @@
+/*
+ * q2d.h -- C ABI of libq2d: transposition-invariant 2D-block FP4 quantization
+ * and the FP4 / MXFP8 GEMMs of a linear layer on AMD Instinct MI355X (gfx950).
+ *
+ * The method ("Stable FP4 Training via Transposition-Invariant Block
+ * Quantization"):
+ *   - a tensor is cut into b x b square blocks; each block gets one
+ *     power-of-two scale S = 2^ceil(log2(2M / (Qp - Qn))) from its maximum
+ *     magnitude M, with the E2M1 bounds Qp = 6, Qn = -6, so nothing is
+ *     clipped (Sec. 3.1; App. D);
+ *   - elements are stored as 4-bit E2M1 codes of x / S, rounded to nearest
+ *     (forward operands) or stochastically with E[round(x)] = x (gradients)
+ *     (Sec. 3.1; App. E);
+ *   - a square block keeps its values and its scale under transposition
+ *     (Sec. 3; App. D), so each operand of Y = X W^T, dX = dY W and
+ *     dW = dY^T X is quantized once and reused transposed (App. C).
+ *     libq2d emits the row-packed and the column-packed copy in one pass;
+ *     both hold the same codes and the same scales;
+ *   - the query/key projections use MXFP8 (E4M3 elements, 1x32 blocks)
+ *     instead (Sec. 3.2; App. C).
+ *
+ * Conventions shared by every entry point:
+ *   - Ownership: the caller allocates every buffer; libq2d never allocates,
+ *     frees or synchronizes.  Sizes come from q2d_tensor_init.
+ *   - Pointers: inputs x and outputs C are device pointers; code and scale
+ *     buffers are device pointers; seg_offsets arrays are device pointers;
+ *     descriptors (q2d_tensor) live in host memory.
+ *   - Ordering: all work is enqueued on `stream` (0 = the null stream) and
+ *     is valid in stream order.  No call blocks the host.
+ *   - Errors: argument errors are detected on the host before any launch and
+ *     returned as a status; nothing is printed, no exception crosses the ABI.
+ *     A failed launch returns Q2D_ELAUNCH.  Data-dependent conditions are not
+ *     errors: a block holding a NaN or an infinity gets scale byte 0xFF (the
+ *     E8M0 NaN) and all-zero codes.
+ *   - Thread safety: the library keeps no mutable state.
+ */
+#ifndef Q2D_H
+#define Q2D_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    Q2D_OK = 0,
+    Q2D_EINVAL = 1,          /* bad argument: null pointer, size, stride, alignment, shape mismatch */
+    Q2D_EUNSUPPORTED = 2,    /* valid request this build does not implement (e.g. block != 32) */
+    Q2D_ELAUNCH = 3          /* the HIP runtime rejected a kernel launch */
+} q2d_status;
+
+typedef enum { Q2D_F32 = 0, Q2D_BF16 = 1 } q2d_dtype;
+
+typedef enum {
+    Q2D_RTN = 0,             /* round to nearest, ties to the even E2M1 code (App. E, forward) */
+    Q2D_SR = 1               /* stochastic rounding, Philox4x32-10, 16 bits per element (App. E) */
+} q2d_round;
+
+typedef enum {
+    Q2D_FMT_FP4_2D = 0,      /* E2M1 codes, one E8M0 scale per 32x32 block (Sec. 3) */
+    Q2D_FMT_MXFP8 = 1        /* E4M3 codes, one E8M0 scale per 1x32 block (Sec. 3.2) */
+} q2d_fmt;
+
+/*
+ * A quantized R x C matrix in both orientations.
+ *
+ * FP4_2D (Sec. 3; App. D):
+ *   codes    [rows][ld_codes] bytes; byte (r, c/2), low nibble = even c.
+ *            Bytes up to roundup(cols,128)/2 of each row are written (padding 0).
+ *   codes_t  [cols][ld_codes_t] bytes; byte (c, r/2), low nibble = even r.
+ *            Bytes up to roundup(rows,128)/2 of each row are written.
+ *   scales   [ceil(rows/32)][ld_scales]: E8M0 byte e+127 of block (r/32, c/32);
+ *            entries up to roundup(cols,128)/32 are written (padding 0x00).
+ *   scales_t [ceil(cols/32)][ld_scales_t]: the same bytes transposed,
+ *            entries up to roundup(rows,128)/32 written.  Every value in
+ *            scales_t equals the one in scales: the transposition invariance.
+ *   A nibble is sign << 3 | m with m indexing {0, .5, 1, 1.5, 2, 3, 4, 6}.
+ *
+ * MXFP8 (Sec. 3.2):
+ *   codes    [rows][ld_codes] E4M3 bytes, scales [rows][ld_scales]: one scale
+ *            per 1x32 block along columns (K = cols);
+ *   codes_t  [cols][ld_codes_t], scales_t [cols][ld_scales_t]: the 32x1
+ *            (column-direction) quantization, stored transposed (K = rows).
+ *            Unlike FP4_2D, the two copies have different scales.
+ *   Rows are padded to multiples of 128 bytes (codes) / 4 bytes (scales) as
+ *   for FP4_2D, padding 0.
+ *
+ * All leading dimensions are in bytes.  Pointers may be NULL for an
+ * orientation the caller does not need (codes with scales, codes_t with
+ * scales_t); GEMMs need the orientation their transpose flag selects.
+ */
+typedef struct {
+    int32_t fmt;             /* q2d_fmt */
+    int32_t block;           /* block edge; 32 */
+    int64_t rows, cols;      /* logical shape R x C */
+    uint8_t *codes;    int64_t ld_codes;
+    uint8_t *codes_t;  int64_t ld_codes_t;
+    uint8_t *scales;   int64_t ld_scales;
+    uint8_t *scales_t; int64_t ld_scales_t;
+} q2d_tensor;
+
+/*
+ * Fill `t` with the layout of an R x C matrix (fmt, block, shape and the
+ * minimal leading dimensions; pointers set to NULL) and, if `bytes` is not
+ * NULL, the byte sizes of its four buffers {codes, codes_t, scales, scales_t}.
+ * Host only.  Q2D_EINVAL for rows or cols <= 0; Q2D_EUNSUPPORTED for a block
+ * other than 32.
+ */
+q2d_status q2d_tensor_init(q2d_tensor *t, q2d_fmt fmt, int64_t rows, int64_t cols,
+                           int32_t block, int64_t bytes[4]);
+
+/*
+ * 2D-block FP4 quantization (Sec. 3, Sec. 3.1; App. D, App. E).
+ *
+ * x        device pointer to element (0, 0) of an R x C matrix of dtype `dt`;
+ *          element (r, c) is x[r*stride_r + c*stride_c] (strides in elements,
+ *          > 0).  Views are allowed: stride_c == 1 (row-major) and
+ *          stride_r == 1 (a transposed view) take the fast path, other strides
+ *          a slower element-wise path.
+ * block    32.
+ * mode     Q2D_RTN or Q2D_SR.  For SR the 16 random bits of the element with
+ *          storage index i = r*stride_r + c*stride_c are half (i & 1) of word
+ *          (i & 7) >> 1 of Philox4x32-10 with counter (g lo, g hi, offset lo,
+ *          offset hi), g = i >> 3, and key (seed lo, seed hi); the magnitude
+ *          rounds up iff floor(2^16 * d / delta) + r16 >= 2^16 (d = distance to
+ *          the grid point below, delta = grid spacing).  A transposed view
+ *          therefore draws the same bits as the matrix it views.
+ * out      descriptor from q2d_tensor_init(FP4_2D, rows, cols, 32) with device
+ *          buffers attached; ld_* may exceed the minimum.  At least one of
+ *          codes / codes_t must be set.  Buffers must be 16-byte aligned and
+ *          leading dimensions multiples of 16 (codes) and 4 (scales).
+ */
+q2d_status q2d_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols,
+                        int64_t stride_r, int64_t stride_c, int32_t block, q2d_round mode,
+                        uint64_t seed, uint64_t offset, q2d_tensor *out, hipStream_t stream);
+
+/*
+ * MXFP8 quantization for the query/key projections (Sec. 3.2; App. C):
+ * E4M3 codes rounded to nearest even, one truncation-free E8M0 scale per 1x32
+ * block (smallest power of two S with 448 * S >= block maximum).  The rowwise
+ * copy (blocks along columns) goes to codes/scales, the colwise copy (blocks
+ * along rows, stored transposed) to codes_t/scales_t, both in one pass.
+ * Arguments as for q2d_quantize; out from q2d_tensor_init(MXFP8, ...).
+ */
+q2d_status mxfp8_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols,
+                          int64_t stride_r, int64_t stride_c, q2d_tensor *out,
+                          hipStream_t stream);
+
+/*
+ * C[M][N] (+)= op(A) . op(B)^T on quantized operands (Sec. 3, "Application to
+ * linear layers"; App. C), fp32 accumulation on scaled MFMA.
+ *
+ * op(X) = X (uses codes/scales; K = X.cols) when transX == 0, or X^T (uses
+ * codes_t/scales_t; K = X.rows) when transX == 1.  M = rows of op(A),
+ * N = rows of op(B); both must have the same K and the same fmt.
+ *   forward     Y  = X  W^T : q2d_gemm(X, 0, W, 0, ...)
+ *   data grad   dX = dY W   : q2d_gemm(dY, 0, W, 1, ...)
+ *   weight grad dW = dY^T X : q2d_gemm(dY, 1, X, 1, ...)
+ * C        device pointer, row-major with leading dimension ldc (elements,
+ *          >= N); c_dt Q2D_F32 or Q2D_BF16 (bf16 rounds to nearest even).
+ * accumulate  0: C = result; 1: C += result (read-modify-write in c_dt).
+ */
+q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB,
+                    void *C, q2d_dtype c_dt, int64_t ldc, int accumulate, hipStream_t stream);
+
+/*
+ * Forward pass of a quantized linear layer Y = X W^T (Sec. 3; App. C):
+ * quantizes X [T][K] and W [N][K] (row-major, dtype dt) into qX and qW (both
+ * orientations, kept for the backward pass) and runs the forward GEMM into
+ * Y [T][N] (row-major, ldy = N, dtype y_dt).  The SR streams of X and W use
+ * (seed, offset_x) and (seed, offset_w).
+ */
+q2d_status q2d_linear_fwd(const void *X, const void *W, q2d_dtype dt, int64_t T, int64_t N,
+                          int64_t K, q2d_round mode_x, q2d_round mode_w, uint64_t seed,
+                          uint64_t offset_x, uint64_t offset_w, q2d_tensor *qX, q2d_tensor *qW,
+                          void *Y, q2d_dtype y_dt, hipStream_t stream);
+
+/*
+ * Backward pass of the same layer (Sec. 3; App. C, App. E): quantizes dY [T][N]
+ * into qdY (both orientations) and computes dX = dY W into dX [T][K] and
+ * dW = dY^T X into dW [N][K], reusing the forward's qX and qW transposed with
+ * their unchanged scales (the straight-through estimator passes dY through the
+ * quantizer unchanged).  accumulate_dw: 1 adds into dW.
+ */
+q2d_status q2d_linear_bwd(const void *dY, q2d_dtype dt, const q2d_tensor *qX,
+                          const q2d_tensor *qW, q2d_round mode_dy, uint64_t seed,
+                          uint64_t offset_dy, q2d_tensor *qdY, void *dX, q2d_dtype dx_dt,
+                          void *dW, q2d_dtype dw_dt, int accumulate_dw, hipStream_t stream);
+
+/* Static description of a status code (never NULL). */
+const char *q2d_status_string(q2d_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* Q2D_H */

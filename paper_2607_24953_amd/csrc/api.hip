@@ -1,0 +1,250 @@
+// C ABI of libq2d: argument validation, layout arithmetic and launches on the
+// caller's stream.  No allocation, no synchronization, no printing.
+#include "../../include/q2d.h"
+#include "kernels.hpp"
+
+#include <stdint.h>
+
+namespace {
+
+using namespace q2d;
+
+constexpr int64_t kPadK = 128;     // K extents are padded to the GEMM K-tile
+
+inline int64_t rup(int64_t a, int64_t m) { return (a + m - 1) / m * m; }
+inline int64_t cdiv(int64_t a, int64_t m) { return (a + m - 1) / m; }
+inline bool aligned(const void *p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+struct Layout {
+    int64_t ld_codes, ld_codes_t, ld_scales, ld_scales_t;
+    int64_t rows_codes, rows_codes_t, rows_scales, rows_scales_t;
+};
+
+Layout layout_of(q2d_fmt fmt, int64_t R, int64_t C)
+{
+    Layout l;
+    if (fmt == Q2D_FMT_FP4_2D) {
+        l.ld_codes = rup(C, kPadK) / 2;   l.rows_codes = R;
+        l.ld_codes_t = rup(R, kPadK) / 2; l.rows_codes_t = C;
+        l.ld_scales = rup(C, kPadK) / 32; l.rows_scales = cdiv(R, 32);
+        l.ld_scales_t = rup(R, kPadK) / 32; l.rows_scales_t = cdiv(C, 32);
+    } else {
+        l.ld_codes = rup(C, kPadK);       l.rows_codes = R;
+        l.ld_codes_t = rup(R, kPadK);     l.rows_codes_t = C;
+        l.ld_scales = rup(C, kPadK) / 32; l.rows_scales = R;
+        l.ld_scales_t = rup(R, kPadK) / 32; l.rows_scales_t = C;
+    }
+    return l;
+}
+
+bool valid_dtype(q2d_dtype d) { return d == Q2D_F32 || d == Q2D_BF16; }
+int dtype_bytes(q2d_dtype d) { return d == Q2D_F32 ? 4 : 2; }
+
+// Check one orientation's buffers against the minimal layout.
+bool check_pair(const uint8_t *codes, int64_t ldc, int64_t min_ldc, const uint8_t *scales,
+                int64_t lds, int64_t min_lds)
+{
+    if (!codes) return true;
+    if (!scales) return false;
+    if (ldc < min_ldc || (ldc % 16) != 0 || lds < min_lds || (lds % 4) != 0) return false;
+    return aligned(codes, 16) && aligned(scales, 4);
+}
+
+q2d_status check_tensor(const q2d_tensor *t, q2d_fmt fmt, int64_t R, int64_t C)
+{
+    if (!t) return Q2D_EINVAL;
+    if (t->fmt != fmt || t->rows != R || t->cols != C) return Q2D_EINVAL;
+    if (t->block != 32) return Q2D_EUNSUPPORTED;
+    if (!t->codes && !t->codes_t) return Q2D_EINVAL;
+    const Layout l = layout_of(fmt, R, C);
+    if (!check_pair(t->codes, t->ld_codes, l.ld_codes, t->scales, t->ld_scales, l.ld_scales)) return Q2D_EINVAL;
+    if (!check_pair(t->codes_t, t->ld_codes_t, l.ld_codes_t, t->scales_t, t->ld_scales_t, l.ld_scales_t))
+        return Q2D_EINVAL;
+    return Q2D_OK;
+}
+
+// Build launch arguments; a transposed view (stride_r == 1) is quantized as its
+// row-major storage with the two orientations swapped, which leaves every
+// element's storage index, block and scale unchanged.
+QuantArgs make_quant_args(const void *x, int64_t R, int64_t C, int64_t sr, int64_t sc,
+                          uint64_t seed, uint64_t offset, const q2d_tensor *t)
+{
+    QuantArgs a;
+    const bool swap = (sc != 1 && sr == 1);
+    a.x = x;
+    a.index_base = 0;
+    a.seed = seed;
+    a.offset = offset;
+    if (!swap) {
+        a.rows = R; a.cols = C; a.stride_r = sr; a.stride_c = sc;
+        a.codes = t->codes;       a.ld_codes = t->ld_codes;
+        a.codes_t = t->codes_t;   a.ld_codes_t = t->ld_codes_t;
+        a.scales = t->scales;     a.ld_scales = t->ld_scales;
+        a.scales_t = t->scales_t; a.ld_scales_t = t->ld_scales_t;
+    } else {
+        a.rows = C; a.cols = R; a.stride_r = sc; a.stride_c = sr;
+        a.codes = t->codes_t;     a.ld_codes = t->ld_codes_t;
+        a.codes_t = t->codes;     a.ld_codes_t = t->ld_codes;
+        a.scales = t->scales_t;   a.ld_scales = t->ld_scales_t;
+        a.scales_t = t->scales;   a.ld_scales_t = t->ld_scales;
+    }
+    a.rows_pad = rup(a.rows, 128);
+    a.cols_pad = rup(a.cols, 128);
+    a.nbr = cdiv(a.rows, 32);
+    a.nbc = cdiv(a.cols, 32);
+    return a;
+}
+
+q2d_status check_input(const void *x, q2d_dtype dt, int64_t R, int64_t C, int64_t sr, int64_t sc)
+{
+    if (!x || !valid_dtype(dt) || R <= 0 || C <= 0 || sr <= 0 || sc <= 0) return Q2D_EINVAL;
+    if (!aligned(x, (uintptr_t)dtype_bytes(dt))) return Q2D_EINVAL;
+    if (R > (int64_t(1) << 31) || C > (int64_t(1) << 31)) return Q2D_EUNSUPPORTED;
+    return Q2D_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+q2d_status q2d_tensor_init(q2d_tensor *t, q2d_fmt fmt, int64_t rows, int64_t cols, int32_t block,
+                           int64_t bytes[4])
+{
+    if (!t || rows <= 0 || cols <= 0) return Q2D_EINVAL;
+    if (fmt != Q2D_FMT_FP4_2D && fmt != Q2D_FMT_MXFP8) return Q2D_EINVAL;
+    if (block != 32) return Q2D_EUNSUPPORTED;
+    const Layout l = layout_of(fmt, rows, cols);
+    t->fmt = fmt; t->block = block; t->rows = rows; t->cols = cols;
+    t->codes = t->codes_t = t->scales = t->scales_t = nullptr;
+    t->ld_codes = l.ld_codes; t->ld_codes_t = l.ld_codes_t;
+    t->ld_scales = l.ld_scales; t->ld_scales_t = l.ld_scales_t;
+    if (bytes) {
+        bytes[0] = l.ld_codes * l.rows_codes;
+        bytes[1] = l.ld_codes_t * l.rows_codes_t;
+        bytes[2] = l.ld_scales * l.rows_scales;
+        bytes[3] = l.ld_scales_t * l.rows_scales_t;
+    }
+    return Q2D_OK;
+}
+
+q2d_status q2d_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols, int64_t stride_r,
+                        int64_t stride_c, int32_t block, q2d_round mode, uint64_t seed,
+                        uint64_t offset, q2d_tensor *out, hipStream_t stream)
+{
+    q2d_status s = check_input(x, dt, rows, cols, stride_r, stride_c);
+    if (s != Q2D_OK) return s;
+    if (mode != Q2D_RTN && mode != Q2D_SR) return Q2D_EINVAL;
+    if (block != 32) return Q2D_EUNSUPPORTED;
+    s = check_tensor(out, Q2D_FMT_FP4_2D, rows, cols);
+    if (s != Q2D_OK) return s;
+    const QuantArgs a = make_quant_args(x, rows, cols, stride_r, stride_c, seed, offset, out);
+    if (launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, stream) != hipSuccess) return Q2D_ELAUNCH;
+    return Q2D_OK;
+}
+
+q2d_status mxfp8_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols, int64_t stride_r,
+                          int64_t stride_c, q2d_tensor *out, hipStream_t stream)
+{
+    q2d_status s = check_input(x, dt, rows, cols, stride_r, stride_c);
+    if (s != Q2D_OK) return s;
+    s = check_tensor(out, Q2D_FMT_MXFP8, rows, cols);
+    if (s != Q2D_OK) return s;
+    // The two MXFP8 copies use different block directions, so a transposed
+    // view is not a relabelling of its storage: always read element-wise.
+    QuantArgs a;
+    a.x = x; a.rows = rows; a.cols = cols; a.stride_r = stride_r; a.stride_c = stride_c;
+    a.index_base = 0; a.seed = 0; a.offset = 0;
+    a.codes = out->codes;       a.ld_codes = out->ld_codes;
+    a.codes_t = out->codes_t;   a.ld_codes_t = out->ld_codes_t;
+    a.scales = out->scales;     a.ld_scales = out->ld_scales;
+    a.scales_t = out->scales_t; a.ld_scales_t = out->ld_scales_t;
+    a.rows_pad = rup(rows, 128); a.cols_pad = rup(cols, 128);
+    a.nbr = rows; a.nbc = cols;
+    if (launch_mxfp8_quantize(a, dtype_bytes(dt), stream) != hipSuccess) return Q2D_ELAUNCH;
+    return Q2D_OK;
+}
+
+q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, void *C,
+                    q2d_dtype c_dt, int64_t ldc, int accumulate, hipStream_t stream)
+{
+    if (!A || !B || !C || !valid_dtype(c_dt)) return Q2D_EINVAL;
+    if ((transA != 0 && transA != 1) || (transB != 0 && transB != 1)) return Q2D_EINVAL;
+    if (accumulate != 0 && accumulate != 1) return Q2D_EINVAL;
+    if (A->fmt != B->fmt || (A->fmt != Q2D_FMT_FP4_2D && A->fmt != Q2D_FMT_MXFP8)) return Q2D_EINVAL;
+    if (A->block != 32 || B->block != 32) return Q2D_EUNSUPPORTED;
+    if (A->rows <= 0 || A->cols <= 0 || B->rows <= 0 || B->cols <= 0) return Q2D_EINVAL;
+    const int64_t M = transA ? A->cols : A->rows, Ka = transA ? A->rows : A->cols;
+    const int64_t N = transB ? B->cols : B->rows, Kb = transB ? B->rows : B->cols;
+    if (Ka != Kb || ldc < N) return Q2D_EINVAL;
+    if (!aligned(C, (uintptr_t)dtype_bytes(c_dt))) return Q2D_EINVAL;
+    const q2d_fmt fmt = (q2d_fmt)A->fmt;
+    const Layout la = layout_of(fmt, A->rows, A->cols), lb = layout_of(fmt, B->rows, B->cols);
+    GemmArgs g;
+    if (!transA) {
+        if (!check_pair(A->codes, A->ld_codes, la.ld_codes, A->scales, A->ld_scales, la.ld_scales) || !A->codes)
+            return Q2D_EINVAL;
+        g.a = A->codes; g.lda = A->ld_codes; g.sa = A->scales; g.ldsa = A->ld_scales;
+    } else {
+        if (!check_pair(A->codes_t, A->ld_codes_t, la.ld_codes_t, A->scales_t, A->ld_scales_t, la.ld_scales_t) ||
+            !A->codes_t)
+            return Q2D_EINVAL;
+        g.a = A->codes_t; g.lda = A->ld_codes_t; g.sa = A->scales_t; g.ldsa = A->ld_scales_t;
+    }
+    if (!transB) {
+        if (!check_pair(B->codes, B->ld_codes, lb.ld_codes, B->scales, B->ld_scales, lb.ld_scales) || !B->codes)
+            return Q2D_EINVAL;
+        g.b = B->codes; g.ldb = B->ld_codes; g.sb = B->scales; g.ldsb = B->ld_scales;
+    } else {
+        if (!check_pair(B->codes_t, B->ld_codes_t, lb.ld_codes_t, B->scales_t, B->ld_scales_t, lb.ld_scales_t) ||
+            !B->codes_t)
+            return Q2D_EINVAL;
+        g.b = B->codes_t; g.ldb = B->ld_codes_t; g.sb = B->scales_t; g.ldsb = B->ld_scales_t;
+    }
+    g.c = C; g.ldc = ldc;
+    g.M = M; g.N = N; g.K = rup(Ka, kPadK);
+    g.accumulate = accumulate;
+    if (launch_gemm(g, fmt == Q2D_FMT_FP4_2D ? kFmtFp4Block2D : kFmtMxfp8, c_dt == Q2D_BF16, stream) != hipSuccess)
+        return Q2D_ELAUNCH;
+    return Q2D_OK;
+}
+
+q2d_status q2d_linear_fwd(const void *X, const void *W, q2d_dtype dt, int64_t T, int64_t N, int64_t K,
+                          q2d_round mode_x, q2d_round mode_w, uint64_t seed, uint64_t offset_x,
+                          uint64_t offset_w, q2d_tensor *qX, q2d_tensor *qW, void *Y, q2d_dtype y_dt,
+                          hipStream_t stream)
+{
+    if (!qX || !qW || !qX->codes || !qW->codes) return Q2D_EINVAL;
+    q2d_status s = q2d_quantize(X, dt, T, K, K, 1, 32, mode_x, seed, offset_x, qX, stream);
+    if (s != Q2D_OK) return s;
+    s = q2d_quantize(W, dt, N, K, K, 1, 32, mode_w, seed, offset_w, qW, stream);
+    if (s != Q2D_OK) return s;
+    return q2d_gemm(qX, 0, qW, 0, Y, y_dt, N, 0, stream);
+}
+
+q2d_status q2d_linear_bwd(const void *dY, q2d_dtype dt, const q2d_tensor *qX, const q2d_tensor *qW,
+                          q2d_round mode_dy, uint64_t seed, uint64_t offset_dy, q2d_tensor *qdY, void *dX,
+                          q2d_dtype dx_dt, void *dW, q2d_dtype dw_dt, int accumulate_dw, hipStream_t stream)
+{
+    if (!qX || !qW || !qdY) return Q2D_EINVAL;
+    const int64_t T = qX->rows, K = qX->cols, N = qW->rows;
+    if (qW->cols != K || qdY->rows != T || qdY->cols != N) return Q2D_EINVAL;
+    if (!qdY->codes || !qdY->codes_t || !qX->codes_t || !qW->codes_t) return Q2D_EINVAL;
+    q2d_status s = q2d_quantize(dY, dt, T, N, N, 1, 32, mode_dy, seed, offset_dy, qdY, stream);
+    if (s != Q2D_OK) return s;
+    s = q2d_gemm(qdY, 0, qW, 1, dX, dx_dt, K, 0, stream);
+    if (s != Q2D_OK) return s;
+    return q2d_gemm(qdY, 1, qX, 1, dW, dw_dt, K, accumulate_dw, stream);
+}
+
+const char *q2d_status_string(q2d_status s)
+{
+    switch (s) {
+    case Q2D_OK: return "ok";
+    case Q2D_EINVAL: return "invalid argument";
+    case Q2D_EUNSUPPORTED: return "unsupported configuration";
+    case Q2D_ELAUNCH: return "kernel launch failed";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

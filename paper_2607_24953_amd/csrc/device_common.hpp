@@ -1,0 +1,116 @@
+// Device-side helpers shared by the libq2d kernels (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace q2d {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float bits_f(uint32_t u) { return __uint_as_float(u); }
+__device__ __forceinline__ uint32_t f_bits(float f) { return __float_as_uint(f); }
+
+// Philox4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC 2011): two 32x32->64
+// multiplies per round, key bumped by the Weyl constants between rounds.  The
+// key is wave-uniform, so the bumps stay scalar.
+__device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                              uint32_t k0, uint32_t k1, uint32_t out[4])
+{
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+        const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+        const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+        const uint32_t n0 = hi1 ^ c1 ^ k0;
+        const uint32_t n2 = hi0 ^ c3 ^ k1;
+        c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+// The 16-bit stochastic-rounding draw of storage index idx: half (idx & 1) of
+// word (idx & 7) >> 1 of the block for counter (idx >> 3, offset).
+__device__ __forceinline__ uint32_t sr_draw(uint64_t idx, uint32_t k0, uint32_t k1,
+                                            uint32_t off_lo, uint32_t off_hi)
+{
+    const uint64_t g = idx >> 3;
+    uint32_t w[4];
+    philox4x32_10((uint32_t)g, (uint32_t)(g >> 32), off_lo, off_hi, k0, k1, w);
+    const uint32_t j = (uint32_t)idx & 7u;
+    const uint32_t word = (j & 4u) ? ((j & 2u) ? w[3] : w[2]) : ((j & 2u) ? w[1] : w[0]);
+    return (word >> ((j & 1u) * 16u)) & 0xFFFFu;
+}
+
+// Truncation-free E2M1 block exponent from the block maximum's float32 bit
+// pattern (sign cleared): the smallest e with 6 * 2^e >= M.  For M = 1.f * 2^p
+// that is p - 2, plus one when f > 1.5; subnormal and tiny maxima clamp to -127.
+__device__ __forceinline__ int fp4_block_exponent(uint32_t amax_bits)
+{
+    const int eb = (int)(amax_bits >> 23);
+    if (eb == 0) return -127;
+    const int e = eb - 129 + ((amax_bits & 0x7FFFFFu) > 0x400000u ? 1 : 0);
+    return e < -127 ? -127 : e;
+}
+
+// Same rule for E4M3 (largest magnitude 448 = 1.75 * 2^8): e = p - 8, plus one
+// when f > 1.75.
+__device__ __forceinline__ int fp8_block_exponent(uint32_t amax_bits)
+{
+    const int eb = (int)(amax_bits >> 23);
+    if (eb == 0) return -127;
+    const int e = eb - 135 + ((amax_bits & 0x7FFFFFu) > 0x600000u ? 1 : 0);
+    return e < -127 ? -127 : e;
+}
+
+// 2^-e as a float for e in [-127, 126].
+__device__ __forceinline__ float inv_pow2(int e) { return bits_f((uint32_t)(127 - e) << 23); }
+
+// E2M1 magnitude index of v = |x| / S in [0, 6], round to nearest, ties to even.
+// The grid spacing is 1/2 below 2, 1 on [2, 4) and 2 on [4, 6]; v * (1 / spacing)
+// is exact, so rint (ties to even) of it lands on the neighbouring grid point
+// with the even mantissa bit.
+__device__ __forceinline__ uint32_t e2m1_rtn(float v)
+{
+    const float t = v < 2.0f ? 2.0f : (v < 4.0f ? 1.0f : 0.5f);
+    const int base = v < 2.0f ? 0 : (v < 4.0f ? 2 : 4);
+    return (uint32_t)((int)__builtin_rintf(v * t) + base);
+}
+
+// Stochastic rounding: floor index k plus a carry when F + r16 >= 2^16, with
+// F = floor(2^16 * (v - G[k]) / spacing).  Every step is exact in float32.
+__device__ __forceinline__ uint32_t e2m1_sr(float v, uint32_t r16)
+{
+    const float t = v < 2.0f ? 2.0f : (v < 4.0f ? 1.0f : 0.5f);
+    const int base = v < 2.0f ? 0 : (v < 4.0f ? 2 : 4);
+    const float u = v * t;
+    const float fl = __builtin_floorf(u);
+    const uint32_t F = (uint32_t)((u - fl) * 65536.0f);
+    return (uint32_t)((int)fl + base) + ((F + r16) >> 16);
+}
+
+// E4M3FN code magnitude of v in [0, 448], round to nearest even.  Below 2^-6
+// the spacing is 2^-9 (subnormals); above it the 3-bit mantissa is rounded on
+// the float32 bit pattern.
+__device__ __forceinline__ uint32_t e4m3_rne(float v)
+{
+    if (v < 0.015625f) return (uint32_t)(int)__builtin_rintf(v * 512.0f);
+    uint32_t b = f_bits(v);
+    b += 0x7FFFFu + ((b >> 20) & 1u);
+    return (b >> 20) - (120u << 3);
+}
+
+__device__ __forceinline__ float bf16_to_f(uint16_t h) { return bits_f((uint32_t)h << 16); }
+
+__device__ __forceinline__ uint16_t f_to_bf16_rne(float f)
+{
+    uint32_t b = f_bits(f);
+    if ((b & 0x7F800000u) == 0x7F800000u) return (uint16_t)((b >> 16) | ((b & 0xFFFFu) ? 0x40u : 0u));
+    b += 0x7FFFu + ((b >> 16) & 1u);
+    return (uint16_t)(b >> 16);
+}
+
+}  // namespace q2d

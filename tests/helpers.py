@@ -1,0 +1,45 @@
+"""Shared helpers of the GPU parity tests (comparison only; no method arithmetic)."""
+import numpy as np
+import torch
+
+BUFS = ("codes", "codes_t", "scales", "scales_t")
+
+
+def gpu_buffers(q) -> dict:
+    torch.cuda.synchronize()
+    return {k: getattr(q, k).cpu().numpy() for k in BUFS if getattr(q, k) is not None}
+
+
+def poison(q, value: int = 0xAA):
+    """Fill every output buffer with a marker so that unwritten bytes show up."""
+    for k in BUFS:
+        t = getattr(q, k)
+        if t is not None:
+            t.fill_(value)
+
+
+def assert_same_bytes(got: dict, want: dict, label: str = ""):
+    for k in BUFS:
+        if k not in got:
+            continue
+        g, w = got[k], want[k]
+        assert g.shape == w.shape, (label, k, g.shape, w.shape)
+        if not np.array_equal(g, w):
+            bad = np.argwhere(g != w)
+            r, c = bad[0]
+            raise AssertionError("%s %s: %d bytes differ, first at (%d, %d): gpu %#04x oracle %#04x"
+                                 % (label, k, len(bad), r, c, g[r, c], w[r, c]))
+
+
+def rel_frob(got: np.ndarray, ref: np.ndarray) -> float:
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.linalg.norm(ref)
+    return float(np.linalg.norm(got - ref) / (den if den > 0 else 1.0))
+
+
+def as_oracle_tensor(q, rows, cols, fmt="fp4") -> dict:
+    """Oracle-style dict of a device QTensor (bytes copied to the host)."""
+    d = gpu_buffers(q)
+    d["rows"], d["cols"] = rows, cols
+    return d

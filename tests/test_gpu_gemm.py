@@ -1,0 +1,183 @@
+"""GPU parity of the block-scaled FP4 and MXFP8 GEMMs against the float64 oracle.
+
+Float32 outputs: relative Frobenius error <= 1e-5 (fp32 accumulation of exact
+FP4 x FP4 products).  Bfloat16 outputs: every element within one bf16 rounding
+(2^-8 relative) of the float64 result.  Shapes span several 128 x 128 output
+tiles and ragged M, N and K tails; all four transpose combinations are used,
+the three GEMMs of a linear layer through q2d_linear_fwd/bwd, accumulation,
+and the full 7B workload in the launch configuration of the benchmark (bf16 Y
+and dX, fp32 dW) on sampled output rows.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import as_oracle_tensor, rel_frob
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL = 1e-5
+
+
+@pytest.fixture(scope="module")
+def q2d():
+    import paper_2607_24953_amd as q
+    return q
+
+
+def quant(q2d, x, mode, seed=0, offset=0):
+    q = q2d.q2d_quantize(x, mode, seed, offset)
+    return q, as_oracle_tensor(q, x.shape[0], x.shape[1])
+
+
+def check_bf16(got, ref):
+    """bf16 output = RNE(fp32 accumulation): within 2^-9 |ref| of the fp32 value, which is
+    itself within the fp32 accumulation error (taken as 1e-5 * rms(ref)) of the exact result."""
+    got = got.float().cpu().numpy().astype(np.float64)
+    err = np.abs(got - ref)
+    rms = float(np.sqrt(np.mean(ref * ref))) if ref.size else 0.0
+    tol = np.abs(ref) * 2.0 ** -8 + 1e-5 * rms + 1e-38
+    assert np.all(err <= tol), float((err / tol).max())
+
+
+GEMM_SHAPES = [(128, 256, 256), (300, 200, 160), (257, 129, 96), (1, 1, 32), (64, 640, 1000),
+               (1000, 300, 2000), (384, 512, 4096)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 1), (1, 0)])
+def test_gemm_fp4(q2d, M, N, K, ta, tb):
+    a_shape = (K, M) if ta else (M, K)
+    b_shape = (K, N) if tb else (N, K)
+    A = synth.normal(a_shape, 1.0, M + K, torch.bfloat16, device=DEV)
+    B = synth.normal(b_shape, 0.02, N + K + 1, torch.bfloat16, device=DEV)
+    qa, oa = quant(q2d, A, "sr", 1, 0)
+    qb, ob = quant(q2d, B, "rtn")
+    ref = oracle.gemm(oracle.operand(oa, bool(ta)), oracle.operand(ob, bool(tb)))
+    c32 = q2d.q2d_gemm(qa, ta, qb, tb, out_dtype=torch.float32)
+    assert rel_frob(c32.cpu().numpy(), ref) <= TOL
+    c16 = q2d.q2d_gemm(qa, ta, qb, tb, out_dtype=torch.bfloat16)
+    check_bf16(c16, ref)
+
+
+def test_gemm_accumulate_and_ldc(q2d):
+    A = synth.normal((200, 320), 1.0, 1, torch.bfloat16, device=DEV)
+    B = synth.normal((150, 320), 1.0, 2, torch.bfloat16, device=DEV)
+    qa, oa = quant(q2d, A, "rtn")
+    qb, ob = quant(q2d, B, "rtn")
+    ref = oracle.gemm(oracle.operand(oa, False), oracle.operand(ob, False))
+    big = torch.randn((200, 160), device=DEV, dtype=torch.float32)
+    c0 = big[:, :150].clone()
+    q2d.q2d_gemm(qa, 0, qb, 0, out=big[:, :150], accumulate=True)
+    assert rel_frob(big[:, :150].cpu().numpy(), ref + c0.cpu().numpy().astype(np.float64)) <= TOL
+
+
+def test_gemm_unit_scales_exact(q2d):
+    """All scales 2^0: the GEMM is an exact integer matmul of 2 * E2M1 values."""
+    rng = np.random.default_rng(4)
+    g = np.array([0, .5, 1, 1.5, 2, 3, 4, 6])
+
+    def grid(R, C):
+        x = g[rng.integers(0, 8, (R, C))] * rng.choice([-1, 1], (R, C))
+        x[::32, ::32] = 6.0
+        return torch.from_numpy(x.astype(np.float32)).to(DEV)
+    A, B = grid(256, 512), grid(192, 512)
+    qa, _ = quant(q2d, A, "rtn")
+    qb, _ = quant(q2d, B, "rtn")
+    c = q2d.q2d_gemm(qa, 0, qb, 0).cpu().numpy().astype(np.float64)
+    ai = (2 * A.cpu().numpy()).astype(np.int64)
+    bi = (2 * B.cpu().numpy()).astype(np.int64)
+    assert np.array_equal(c * 4, (ai @ bi.T).astype(np.float64))
+
+
+@pytest.mark.parametrize("T,N,K", [(128, 256, 256), (96, 300, 200), (512, 1024, 768)])
+def test_linear_fwd_bwd(q2d, T, N, K):
+    X = synth.normal((T, K), 1.0, 1, torch.bfloat16, device=DEV)
+    W = synth.normal((N, K), 0.02, 2, torch.bfloat16, device=DEV)
+    dY = synth.normal((T, N), 1e-3, 3, torch.bfloat16, device=DEV)
+    Y, qX, qW = q2d.q2d_linear_fwd(X, W, "sr", "sr", seed=9, offset_x=0, offset_w=1,
+                                   y_dtype=torch.float32)
+    dX, dW, qdY = q2d.q2d_linear_bwd(dY, qX, qW, "sr", seed=9, offset_dy=2,
+                                     dx_dtype=torch.float32, dw_dtype=torch.float32)
+    ox = oracle.quantize_fp4_2d(X.cpu(), "sr", 9, 0)
+    ow = oracle.quantize_fp4_2d(W.cpu(), "sr", 9, 1)
+    ody = oracle.quantize_fp4_2d(dY.cpu(), "sr", 9, 2)
+    for name, gq, oq in (("X", qX, ox), ("W", qW, ow), ("dY", qdY, ody)):
+        got = as_oracle_tensor(gq, oq["rows"], oq["cols"])
+        for k in ("codes", "codes_t", "scales", "scales_t"):
+            assert np.array_equal(got[k], oq[k]), (name, k)
+    ref = oracle.linear(ox, ow, ody)
+    assert rel_frob(Y.cpu().numpy(), ref["Y"]) <= TOL
+    assert rel_frob(dX.cpu().numpy(), ref["dX"]) <= TOL
+    assert rel_frob(dW.cpu().numpy(), ref["dW"]) <= TOL
+
+
+@pytest.mark.parametrize("M,N,K", [(128, 256, 256), (300, 200, 160), (1000, 300, 2000)])
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 1)])
+def test_gemm_mxfp8(q2d, M, N, K, ta, tb):
+    a_shape = (K, M) if ta else (M, K)
+    b_shape = (K, N) if tb else (N, K)
+    A = synth.normal(a_shape, 1.0, 3 * M + K, torch.bfloat16, device=DEV)
+    synth.add_outlier_channels(A, 5, frac=0.02)
+    B = synth.normal(b_shape, 0.02, N + 7, torch.bfloat16, device=DEV)
+    qa = q2d.mxfp8_quantize(A)
+    qb = q2d.mxfp8_quantize(B)
+    oa = oracle.quantize_mxfp8(A.cpu())
+    ob = oracle.quantize_mxfp8(B.cpu())
+    ga, gb = as_oracle_tensor(qa, *A.shape), as_oracle_tensor(qb, *B.shape)
+    for k in ("codes", "codes_t", "scales", "scales_t"):
+        assert np.array_equal(ga[k], oa[k]), k
+        assert np.array_equal(gb[k], ob[k]), k
+    ref = oracle.gemm(oracle.operand(oa, bool(ta), "mxfp8"), oracle.operand(ob, bool(tb), "mxfp8"))
+    c = q2d.q2d_gemm(qa, ta, qb, tb, out_dtype=torch.float32)
+    assert rel_frob(c.cpu().numpy(), ref) <= TOL
+
+
+def _sample_rows(qt_np, trans, rows, fmt="fp4"):
+    """float64 rows `rows` of op(X) from the host copy of a device quantization."""
+    if fmt == "fp4":
+        codes = qt_np["codes_t" if trans else "codes"][rows]
+        scales = qt_np["scales_t" if trans else "scales"]
+        K = qt_np["rows"] if trans else qt_np["cols"]
+        vals = oracle.fp4_values(np.stack([codes & 15, codes >> 4], -1).reshape(len(rows), -1)[:, :K])
+        s = 2.0 ** (scales[np.asarray(rows) // 32][:, np.arange(K) // 32].astype(np.float64) - 127)
+        return vals * s
+    raise ValueError(fmt)
+
+
+def test_full_7b_launch_configuration(q2d):
+    """The benchmark's 15 GEMMs (bf16 Y and dX, fp32 dW) at full size, 48 sampled rows each.
+
+    The quantized operands are checked byte for byte against the oracle in the
+    quantizer tests; here the GEMM of the device codes is compared with the
+    float64 oracle GEMM of the same codes on sampled output rows."""
+    w = synth.dense_7b(device=DEV)
+    rng = np.random.default_rng(0)
+    for lin in w.linears:
+        X, W, dY = w.tensors[lin.x], w.tensors[lin.w], w.tensors[lin.dy]
+        Y, qX, qW = q2d.q2d_linear_fwd(X, W, w.rounding[lin.x], w.rounding[lin.w], seed=w.seed,
+                                       offset_x=0, offset_w=1, y_dtype=torch.bfloat16)
+        dX, dW, qdY = q2d.q2d_linear_bwd(dY, qX, qW, w.rounding[lin.dy], seed=w.seed, offset_dy=2,
+                                         dx_dtype=torch.bfloat16, dw_dtype=torch.float32)
+        torch.cuda.synchronize()
+        ox = as_oracle_tensor(qX, *X.shape)
+        ow = as_oracle_tensor(qW, *W.shape)
+        ody = as_oracle_tensor(qdY, *dY.shape)
+        print("7B linear %s: checking sampled rows" % lin.name, flush=True)
+        Wf = oracle.operand(ow, False)
+        Wt = oracle.operand(ow, True)
+        Xt = oracle.operand(ox, True)
+        rows = np.sort(rng.choice(lin.tokens, 48, replace=False))
+        ref_y = _sample_rows(ox, False, rows) @ Wf.T
+        check_bf16(Y[torch.from_numpy(rows).to(DEV)], ref_y)
+        ref_dx = _sample_rows(ody, False, rows) @ Wt.T
+        check_bf16(dX[torch.from_numpy(rows).to(DEV)], ref_dx)
+        rows_w = np.sort(rng.choice(lin.n_out, 48, replace=False))
+        ref_dw = _sample_rows(ody, True, rows_w) @ Xt.T
+        got_dw = dW[torch.from_numpy(rows_w).to(DEV)].cpu().numpy()
+        assert rel_frob(got_dw, ref_dw) <= TOL
+        del Y, dX, dW, qX, qW, qdY, Wf, Wt, Xt
+    torch.cuda.empty_cache()
