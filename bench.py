@@ -109,15 +109,15 @@ class Step:
                 ev.append(m + (e1,))
 
         for i, (k, t) in enumerate(w.tensors.items()):
-            m = mark("quant", quant_bytes(t))
+            m = mark(("quant", k), quant_bytes(t))
             q2d.q2d_quantize(t, w.rounding[k], w.seed, i, out=self.q[k])
             done(m)
         for lin, (Y, dX, dW) in zip(w.linears, self.out):
             qx, qw, qdy = self.q[lin.x], self.q[lin.w], self.q[lin.dy]
             f = 2.0 * lin.tokens * lin.n_out * lin.k_in
-            m = mark("gemm", f); q2d.q2d_gemm(qx, 0, qw, 0, out=Y); done(m)
-            m = mark("gemm", f); q2d.q2d_gemm(qdy, 0, qw, 1, out=dX); done(m)
-            m = mark("gemm", f); q2d.q2d_gemm(qdy, 1, qx, 1, out=dW); done(m)
+            m = mark(("gemm", lin.name + ".fwd"), f); q2d.q2d_gemm(qx, 0, qw, 0, out=Y); done(m)
+            m = mark(("gemm", lin.name + ".dX"), f); q2d.q2d_gemm(qdy, 0, qw, 1, out=dX); done(m)
+            m = mark(("gemm", lin.name + ".dW"), f); q2d.q2d_gemm(qdy, 1, qx, 1, out=dW); done(m)
         if record:
             self.events = (self.events or []) + ev
 
@@ -184,12 +184,19 @@ def main():
     t_gemm = t_quant = 0.0
     f_gemm = b_quant = 0.0
     n_gemm = 0
-    for kind, work, e0, e1 in step.events:
+    detail = {}
+    for (kind, name), work, e0, e1 in step.events:
         ms = e0.elapsed_time(e1)
+        d = detail.setdefault(name, [0.0, 0.0, 0])
+        d[0] += ms; d[1] += work; d[2] += 1
         if kind == "gemm":
             t_gemm += ms; f_gemm += work; n_gemm += 1
         else:
             t_quant += ms; b_quant += work
+    per_kernel = {}
+    for name, (ms, work, n) in detail.items():
+        rate = work / (ms * 1e-3) / (1e12 if "." in name else 1e9)
+        per_kernel[name] = {"ms": round(ms / n, 4), ("TFLOP/s" if "." in name else "GB/s"): round(rate, 1)}
     gemm_tflops = f_gemm / (t_gemm * 1e-3) / 1e12
     quant_gbs = b_quant / (t_quant * 1e-3) / 1e9
     flops_step = float(w.gemm_flops)
@@ -227,6 +234,7 @@ def main():
                       "traffic": tr_q["bytes_per_launch"] if tr_q else None,
                       "ms_per_step": round(t_quant / args.steps, 4)},
         "gemm_ms_per_step": round(t_gemm / args.steps, 4),
+        "per_kernel": per_kernel,
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens)

@@ -32,6 +32,13 @@ constexpr int kXcds = 8;
 template <int FMT>
 struct Fmt;
 
+// Operand placement measured on gfx950 for v_mfma_scale_f32_32x32x64_f8f6f4:
+// with E2M1 operands (4 VGPRs) lane l holds 32 consecutive K values of K-group
+// l / 32; with E4M3 operands (8 VGPRs) the first 16 bytes of every lane belong
+// to K-group 0 and the last 16 bytes to K-group 1, the two lane halves splitting
+// each group.  In both cases lane half h supplies the scale of K-group h.
+// chunk(ks, half, h) is the 16-byte chunk of the K-tile row that feeds VGPRs
+// 4h..4h+3 of a lane in half `half` for K-substep ks (64 K values).
 template <>
 struct Fmt<kFmtFp4Block2D> {
     static constexpr int kRowBytes = BK / 2;      // 64 bytes of codes per row per K-tile
@@ -39,6 +46,7 @@ struct Fmt<kFmtFp4Block2D> {
     static constexpr int kCbsz = 4;               // E2M1
     static constexpr int kScaleRowShift = 5;      // one scale per 32-row block
     static __device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+    static __device__ __forceinline__ int chunk(int ks, int half, int) { return 2 * ks + half; }
 };
 
 template <>
@@ -48,6 +56,7 @@ struct Fmt<kFmtMxfp8> {
     static constexpr int kCbsz = 0;               // E4M3
     static constexpr int kScaleRowShift = 0;      // one scale per row and K-group
     static __device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
+    static __device__ __forceinline__ int chunk(int ks, int half, int h) { return 4 * ks + 2 * h + half; }
 };
 
 __device__ __forceinline__ void tile_coords(int64_t tiles_m, int64_t tiles_n, int64_t &tm, int64_t &tn)
@@ -158,10 +167,9 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmArgs g, int64_
             for (int i = 0; i < 2; ++i) {
                 const int ra = wm * 64 + i * 32 + (lane & 31);
                 const int rb = wn * 64 + i * 32 + (lane & 31);
-                const int cbyte = ks * 2 * F::kLaneBytes + half * F::kLaneBytes;   // byte offset in the row
 #pragma unroll
                 for (int h = 0; h < F::kLaneBytes / 16; ++h) {
-                    const int ch = cbyte / 16 + h;
+                    const int ch = F::chunk(ks, half, h);
                     const uint4 qa = *reinterpret_cast<const uint4 *>(&As[buf][ra * RB + ((ch ^ F::swz(ra)) * 16)]);
                     const uint4 qb = *reinterpret_cast<const uint4 *>(&Bs[buf][rb * RB + ((ch ^ F::swz(rb)) * 16)]);
                     af[i][4 * h + 0] = (int)qa.x; af[i][4 * h + 1] = (int)qa.y;
@@ -218,6 +226,192 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmArgs g, int64_
         }
 }
 
+// Large-tile FP4 kernel: 256 x 256 output tile, 4 waves of 128 x 128 (4 x 4
+// MFMA tiles, 256 fp32 accumulators per lane held in AGPRs), one wave per
+// SIMD.  Per K-tile of 128 each wave issues 32 MFMAs (about 1000 cycles at the
+// MFMA rate) against 16 KB of LDS operand reads, half the LDS rate.
+//
+// Codes move global -> LDS with gfx950's global_load_lds_dwordx4 (each lane
+// deposits 16 bytes at M0 + 16 * lane), through a ring of kStages LDS stages
+// kept kStages - 1 K-tiles ahead of the MFMAs.  The loads are issued from
+// inline assembly so that the compiler does not serialize them against LDS
+// reads it cannot prove disjoint; completion is tracked by hand with vmcnt
+// (every iteration issues exactly kDmaPerTile loads, past the last K-tile
+// they re-read the last tile into a stage that is never consumed).  The
+// block-scale words are wave-uniform and come through scalar loads.
+constexpr int BM2 = 256, BN2 = 256;
+constexpr int kStages = 4;
+constexpr int kDmaPerTile = 8;      // per wave: 4 for A, 4 for B
+
+__device__ __forceinline__ void lds_dma16(const uint8_t *src, uint32_t lds_addr)
+{
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_addr), "v"(src) : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+
+__device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Scale words are read through the constant address space: they are never
+// written during the kernel, and this keeps them on the scalar path (lgkmcnt)
+// even though the DMA asm statements clobber memory.
+typedef const __attribute__((address_space(4))) uint32_t const_u32;
+__device__ __forceinline__ uint32_t load_scale_word(const uint8_t *p)
+{
+    return *reinterpret_cast<const_u32 *>(reinterpret_cast<uintptr_t>(p));
+}
+
+template <bool BF16OUT>
+__global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArgs g, int64_t tiles_m, int64_t tiles_n)
+{
+    using F = Fmt<kFmtFp4Block2D>;
+    constexpr int RB = F::kRowBytes;                // 64
+    constexpr int TB = BM2 * RB;                    // 16 KB per operand per stage
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages][2][TB];
+
+    int64_t tm, tn;
+    tile_coords(tiles_m, tiles_n, tm, tn);
+    const int64_t m0 = tm * BM2, n0 = tn * BN2;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+    const int half = lane >> 5;
+    const int64_t nk = g.K / BK;
+
+    // DMA j of this wave fills LDS bytes [(4j + wave) * 1024, +1024) of an
+    // operand stage: rows 16 (4j + wave) + lane / 4, physical chunk lane % 4,
+    // i.e. logical chunk (lane % 4) ^ swz(row).
+    const uint8_t *srcA[4];
+    const uint8_t *srcB[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int row = 16 * (4 * j + wave) + (lane >> 2);
+        const int c = (lane & 3) ^ F::swz(row);
+        int64_t ra = m0 + row; ra = ra < g.M ? ra : g.M - 1;
+        int64_t rb = n0 + row; rb = rb < g.N ? rb : g.N - 1;
+        srcA[j] = g.a + ra * g.lda + c * 16;
+        srcB[j] = g.b + rb * g.ldb + c * 16;
+    }
+    const uint32_t lds0 = (uint32_t)(uintptr_t)&smem[0][0][0];
+    auto issue = [&](int64_t t) {
+        const int64_t tt = t < nk ? t : nk - 1;
+        const uint32_t stage = lds0 + (uint32_t)((t % kStages) * 2 * TB);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            lds_dma16(srcA[j] + tt * RB, stage + (4 * j + wave) * 1024);
+            lds_dma16(srcB[j] + tt * RB, stage + TB + (4 * j + wave) * 1024);
+        }
+    };
+
+    // operand reads: rows wm*128 + 32 i + (lane % 32); bits 1..4 come from lane % 32
+    const int sw = F::swz(lane & 31);
+    const int rd_a = (wm * 128 + (lane & 31)) * RB;
+    const int rd_b = (wn * 128 + (lane & 31)) * RB;
+
+    const uint8_t *sa_row[4];
+    const uint8_t *sb_row[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        int64_t ra = m0 + wm * 128 + i * 32; ra = ra < g.M ? ra : g.M - 1;
+        int64_t rb = n0 + wn * 128 + i * 32; rb = rb < g.N ? rb : g.N - 1;
+        sa_row[i] = g.sa + (ra >> 5) * g.ldsa;
+        sb_row[i] = g.sb + (rb >> 5) * g.ldsb;
+    }
+
+    v16f acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+#pragma unroll
+    for (int t = 0; t < kStages - 1; ++t) issue(t);
+
+    uint32_t scA[4], scB[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        scA[i] = load_scale_word(sa_row[i]);
+        scB[i] = load_scale_word(sb_row[i]);
+    }
+
+    for (int64_t kt = 0; kt < nk; ++kt) {
+        // tile kt has landed once at most (kStages - 2) later groups are in flight
+        wait_vmcnt<(kStages - 2) * kDmaPerTile>();
+        block_barrier();
+        issue(kt + kStages - 1);          // refills the stage consumed in iteration kt - 1
+        uint32_t nA[4], nB[4];
+        const int64_t kn = kt + 1 < nk ? kt + 1 : kt;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            nA[i] = load_scale_word(sa_row[i] + kn * 4);
+            nB[i] = load_scale_word(sb_row[i] + kn * 4);
+        }
+        const uint8_t *As = smem[kt % kStages][0];
+        const uint8_t *Bs = smem[kt % kStages][1];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int cofs = ((2 * ks + half) ^ sw) * 16;
+            const int kg8 = 8 * (2 * ks + half);
+            v8i af[4], bf[4];
+            int sa[4], sb[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint4 qa = *reinterpret_cast<const uint4 *>(As + rd_a + i * 32 * RB + cofs);
+                af[i][0] = (int)qa.x; af[i][1] = (int)qa.y; af[i][2] = (int)qa.z; af[i][3] = (int)qa.w;
+                af[i][4] = 0; af[i][5] = 0; af[i][6] = 0; af[i][7] = 0;
+                const uint4 qb = *reinterpret_cast<const uint4 *>(Bs + rd_b + i * 32 * RB + cofs);
+                bf[i][0] = (int)qb.x; bf[i][1] = (int)qb.y; bf[i][2] = (int)qb.z; bf[i][3] = (int)qb.w;
+                bf[i][4] = 0; bf[i][5] = 0; bf[i][6] = 0; bf[i][7] = 0;
+                sa[i] = (int)((scA[i] >> kg8) & 0xFFu);
+                sb[i] = (int)((scB[i] >> kg8) & 0xFFu);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        af[i], bf[j], acc[i][j], F::kCbsz, F::kCbsz, 0, sa[i], 0, sb[j]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) { scA[i] = nA[i]; scB[i] = nB[i]; }
+    }
+    wait_vmcnt<0>();
+
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t col = n0 + wn * 128 + j * 32 + (lane & 31);
+            if (col >= g.N) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+                if (row >= g.M) continue;
+                float v = acc[i][j][r];
+                if (BF16OUT) {
+                    uint16_t *p = reinterpret_cast<uint16_t *>(g.c) + row * g.ldc + col;
+                    if (g.accumulate) v += bf16_to_f(*p);
+                    *p = f_to_bf16_rne(v);
+                } else {
+                    float *p = reinterpret_cast<float *>(g.c) + row * g.ldc + col;
+                    if (g.accumulate) v += *p;
+                    *p = v;
+                }
+            }
+        }
+}
+
+template <bool BF>
+hipError_t launch_256(const GemmArgs &g, hipStream_t s)
+{
+    const int64_t tm = (g.M + BM2 - 1) / BM2, tn = (g.N + BN2 - 1) / BN2;
+    hipLaunchKernelGGL((gemm_fp4_256_kernel<BF>), dim3((unsigned)(tm * tn)), dim3(kThreads), 0, s, g, tm, tn);
+    return hipGetLastError();
+}
+
 template <int FMT, bool BF>
 hipError_t launch_t(const GemmArgs &g, hipStream_t s)
 {
@@ -230,6 +424,9 @@ hipError_t launch_t(const GemmArgs &g, hipStream_t s)
 
 hipError_t launch_gemm(const GemmArgs &g, int fmt, int c_is_bf16, hipStream_t stream)
 {
+    // the 256 x 256 kernel once there are enough output tiles to fill the chip
+    if (fmt == kFmtFp4Block2D && ((g.M + BM2 - 1) / BM2) * ((g.N + BN2 - 1) / BN2) >= 128)
+        return c_is_bf16 ? launch_256<true>(g, stream) : launch_256<false>(g, stream);
     if (fmt == kFmtFp4Block2D)
         return c_is_bf16 ? launch_t<kFmtFp4Block2D, true>(g, stream) : launch_t<kFmtFp4Block2D, false>(g, stream);
     return c_is_bf16 ? launch_t<kFmtMxfp8, true>(g, stream) : launch_t<kFmtMxfp8, false>(g, stream);

@@ -44,7 +44,10 @@ def check_bf16(got, ref):
 
 
 GEMM_SHAPES = [(128, 256, 256), (300, 200, 160), (257, 129, 96), (1, 1, 32), (64, 640, 1000),
-               (1000, 300, 2000), (384, 512, 4096)]
+               (1000, 300, 2000), (384, 512, 4096),
+               # enough 256 x 256 output tiles for the large-tile kernel: ragged M and N,
+               # K shorter than its LDS pipeline (128, 384) and long (2048)
+               (2048, 4096, 128), (2100, 4000, 384), (4096, 2048, 2048)]
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
@@ -131,9 +134,18 @@ def test_gemm_mxfp8(q2d, M, N, K, ta, tb):
     for k in ("codes", "codes_t", "scales", "scales_t"):
         assert np.array_equal(ga[k], oa[k]), k
         assert np.array_equal(gb[k], ob[k]), k
-    ref = oracle.gemm(oracle.operand(oa, bool(ta), "mxfp8"), oracle.operand(ob, bool(tb), "mxfp8"))
-    c = q2d.q2d_gemm(qa, ta, qb, tb, out_dtype=torch.float32)
-    assert rel_frob(c.cpu().numpy(), ref) <= TOL
+    a64 = oracle.operand(oa, bool(ta), "mxfp8")
+    b64 = oracle.operand(ob, bool(tb), "mxfp8")
+    ref = oracle.gemm(a64, b64)
+    c = q2d.q2d_gemm(qa, ta, qb, tb, out_dtype=torch.float32).cpu().numpy().astype(np.float64)
+    # The E4M3 scaled MFMA does not round the sum of its 64 products exactly to
+    # fp32: it keeps about 13 bits below the instruction's largest product
+    # (measured on gfx950: 1 + 2^-k is exact for k <= 13, the 2^-k term is lost
+    # for k >= 14; the E2M1 form is exact).  Elementwise bound
+    # 2^-11 * (|A| |B|^T) covers that and the fp32 accumulation across K.
+    bound = 2.0 ** -11 * (np.abs(a64) @ np.abs(b64).T) + 1e-30
+    assert np.all(np.abs(c - ref) <= bound), float((np.abs(c - ref) / bound).max())
+    assert rel_frob(c, ref) <= 5e-4
 
 
 def _sample_rows(qt_np, trans, rows, fmt="fp4"):
