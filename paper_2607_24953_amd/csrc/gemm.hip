@@ -232,20 +232,40 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmArgs g, int64_
 // MFMA rate) against 16 KB of LDS operand reads, half the LDS rate.
 //
 // Codes move global -> LDS with gfx950's global_load_lds_dwordx4 (each lane
-// deposits 16 bytes at M0 + 16 * lane), through a ring of kStages LDS stages
-// kept kStages - 1 K-tiles ahead of the MFMAs.  The loads are issued from
-// inline assembly so that the compiler does not serialize them against LDS
-// reads it cannot prove disjoint; completion is tracked by hand with vmcnt
-// (every iteration issues exactly kDmaPerTile loads, past the last K-tile
-// they re-read the last tile into a stage that is never consumed).  The
-// block-scale words are wave-uniform and come through scalar loads.
+// deposits 16 bytes at M0 + 16 * lane) and the block-scale words with
+// global_load_lds_dword, through a ring of kStages LDS stages kept kStages - 1
+// K-tiles ahead of the MFMAs.  The loads are issued from inline assembly so
+// that the compiler does not serialize them against LDS reads it cannot prove
+// disjoint; completion is tracked by hand with vmcnt: every iteration issues
+// exactly kDmaPerTile loads per wave (past the last K-tile they re-read it into
+// a stage that is never consumed).
 constexpr int BM2 = 256, BN2 = 256;
 constexpr int kStages = 4;
-constexpr int kDmaPerTile = 8;      // per wave: 4 for A, 4 for B
+constexpr int kDmaPerTile = 9;      // per wave: 4 for A, 4 for B, 1 for the scale words
+constexpr int kCodeBytes = BM2 * 64;                  // 16 KB per operand per stage
+constexpr int kStageBytes = 2 * kCodeBytes + 1024;    // + 4 waves x 256 B of scale words
 
-__device__ __forceinline__ void lds_dma16(const uint8_t *src, uint32_t lds_addr)
+// Wave-uniform 64-bit value (moves it to SGPRs).
+__device__ __forceinline__ uint64_t uniform64(uint64_t v)
 {
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_addr), "v"(src) : "memory");
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// global -> LDS, 16 bytes per lane at M0 + 16 * lane; address = sbase + voff
+// with a wave-uniform base
+__device__ __forceinline__ void lds_dma16(const uint8_t *sbase, uint32_t voff, uint32_t lds_addr)
+{
+    const uint64_t base = uniform64(reinterpret_cast<uint64_t>(sbase));
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_addr), "v"(voff), "s"(base)
+                 : "memory");
+}
+
+// global -> LDS, 4 bytes per lane at M0 + 4 * lane, per-lane 64-bit address
+__device__ __forceinline__ void lds_dma4(const uint8_t *src, uint32_t lds_addr)
+{
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(lds_addr), "v"(src) : "memory");
 }
 
 template <int N>
@@ -253,71 +273,111 @@ __device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)
 
 __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-// Scale words are read through the constant address space: they are never
-// written during the kernel, and this keeps them on the scalar path (lgkmcnt)
-// even though the DMA asm statements clobber memory.
-typedef const __attribute__((address_space(4))) uint32_t const_u32;
-__device__ __forceinline__ uint32_t load_scale_word(const uint8_t *p)
+__device__ __forceinline__ void grouped_coords32(int t, int tiles_m, int tiles_n, int &tm, int &tn)
 {
-    return *reinterpret_cast<const_u32 *>(reinterpret_cast<uintptr_t>(p));
+    const int span = kGroupM * tiles_n;
+    const int grp = t / span;
+    const int first = grp * kGroupM;
+    const int gsz = (tiles_m - first) < kGroupM ? (tiles_m - first) : kGroupM;
+    const int in = t - grp * span;
+    tm = first + in % gsz;
+    tn = in / gsz;
 }
 
-template <bool BF16OUT>
-__global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArgs g, int64_t tiles_m, int64_t tiles_n)
+// Write a wave's 128 x 128 accumulator block (4 x 4 MFMA tiles) to C; CHECK
+// masks rows >= M and columns >= N.  bf16 output rounds to nearest even.
+template <bool BF16OUT, bool ACC, bool CHECK>
+__device__ __forceinline__ void store_tile(v16f (&acc)[4][4], const GemmArgs &g, int64_t row0, int64_t col0)
+{
+    const int esize = BF16OUT ? 2 : 4;
+    const int64_t ldc_bytes = g.ldc * esize;
+    uint8_t *cbase = reinterpret_cast<uint8_t *>(g.c) + row0 * ldc_bytes + col0 * esize;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int roff = i * 32 + 8 * (r >> 2) + (r & 3);
+            uint8_t *prow = cbase + roff * ldc_bytes;
+            if (CHECK && row0 + roff >= g.M) continue;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (CHECK && col0 + j * 32 >= g.N) continue;
+                float v = acc[i][j][r];
+                if (BF16OUT) {
+                    __bf16 *p = reinterpret_cast<__bf16 *>(prow + j * 32 * 2);
+                    if (ACC) v += (float)*p;
+                    *p = (__bf16)v;
+                } else {
+                    float *p = reinterpret_cast<float *>(prow + j * 32 * 4);
+                    if (ACC) v += *p;
+                    *p = v;
+                }
+            }
+            // keep the scheduler from hoisting all 256 accumulator reads at once
+            // (they would not fit the VGPR file and would spill)
+            __builtin_amdgcn_sched_barrier(0);
+        }
+}
+
+template <bool BF16OUT, bool ACC>
+__global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArgs g, int tiles_m, int tiles_n)
 {
     using F = Fmt<kFmtFp4Block2D>;
     constexpr int RB = F::kRowBytes;                // 64
-    constexpr int TB = BM2 * RB;                    // 16 KB per operand per stage
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages][2][TB];
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];
 
-    int64_t tm, tn;
-    tile_coords(tiles_m, tiles_n, tm, tn);
-    const int64_t m0 = tm * BM2, n0 = tn * BN2;
+    int64_t tm64, tn64;
+    tile_coords(tiles_m, tiles_n, tm64, tn64);
+    const int tm = (int)tm64, tn = (int)tn64;
+    const int64_t m0 = (int64_t)tm * BM2, n0 = (int64_t)tn * BN2;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     const int half = lane >> 5;
-    const int64_t nk = g.K / BK;
+    const uint32_t nk = (uint32_t)(g.K / BK);
 
-    // DMA j of this wave fills LDS bytes [(4j + wave) * 1024, +1024) of an
-    // operand stage: rows 16 (4j + wave) + lane / 4, physical chunk lane % 4,
-    // i.e. logical chunk (lane % 4) ^ swz(row).
-    const uint8_t *srcA[4];
-    const uint8_t *srcB[4];
+    // DMA j of this wave fills bytes [(4j + wave) * 1024, +1024) of an operand
+    // stage: rows 16 (4j + wave) + lane / 4, physical chunk lane % 4.
+    uint32_t offA[4], offB[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         const int row = 16 * (4 * j + wave) + (lane >> 2);
         const int c = (lane & 3) ^ F::swz(row);
         int64_t ra = m0 + row; ra = ra < g.M ? ra : g.M - 1;
         int64_t rb = n0 + row; rb = rb < g.N ? rb : g.N - 1;
-        srcA[j] = g.a + ra * g.lda + c * 16;
-        srcB[j] = g.b + rb * g.ldb + c * 16;
+        offA[j] = (uint32_t)(ra * g.lda + c * 16);
+        offB[j] = (uint32_t)(rb * g.ldb + c * 16);
     }
-    const uint32_t lds0 = (uint32_t)(uintptr_t)&smem[0][0][0];
-    auto issue = [&](int64_t t) {
-        const int64_t tt = t < nk ? t : nk - 1;
-        const uint32_t stage = lds0 + (uint32_t)((t % kStages) * 2 * TB);
+    // scale words: lanes 0-3 the wave's four A block rows, lanes 4-7 its four B block rows
+    const uint8_t *srcS;
+    {
+        const int q = lane & 7;
+        if (q < 4) {
+            int64_t ra = m0 + wm * 128 + q * 32; ra = ra < g.M ? ra : g.M - 1;
+            srcS = g.sa + (ra >> 5) * g.ldsa;
+        } else {
+            int64_t rb = n0 + wn * 128 + (q - 4) * 32; rb = rb < g.N ? rb : g.N - 1;
+            srcS = g.sb + (rb >> 5) * g.ldsb;
+        }
+    }
+    const uint32_t lds0 = (uint32_t)(uintptr_t)&smem[0];
+    // K-tile t into stage t % kStages; past the last K-tile re-read the last one
+    auto issue = [&](uint32_t t) {
+        const uint32_t tt = t < nk ? t : nk - 1;
+        const uint32_t stage = lds0 + (t % kStages) * kStageBytes;
+        const uint8_t *ba = g.a + tt * RB;
+        const uint8_t *bb = g.b + tt * RB;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            lds_dma16(srcA[j] + tt * RB, stage + (4 * j + wave) * 1024);
-            lds_dma16(srcB[j] + tt * RB, stage + TB + (4 * j + wave) * 1024);
+            lds_dma16(ba, offA[j], stage + (4 * j + wave) * 1024);
+            lds_dma16(bb, offB[j], stage + kCodeBytes + (4 * j + wave) * 1024);
         }
+        lds_dma4(srcS + tt * 4, stage + 2 * kCodeBytes + wave * 256);
     };
 
-    // operand reads: rows wm*128 + 32 i + (lane % 32); bits 1..4 come from lane % 32
     const int sw = F::swz(lane & 31);
     const int rd_a = (wm * 128 + (lane & 31)) * RB;
-    const int rd_b = (wn * 128 + (lane & 31)) * RB;
-
-    const uint8_t *sa_row[4];
-    const uint8_t *sb_row[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        int64_t ra = m0 + wm * 128 + i * 32; ra = ra < g.M ? ra : g.M - 1;
-        int64_t rb = n0 + wn * 128 + i * 32; rb = rb < g.N ? rb : g.N - 1;
-        sa_row[i] = g.sa + (ra >> 5) * g.ldsa;
-        sb_row[i] = g.sb + (rb >> 5) * g.ldsb;
-    }
+    const int rd_b = kCodeBytes + (wn * 128 + (lane & 31)) * RB;
 
     v16f acc[4][4];
 #pragma unroll
@@ -328,29 +388,18 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArg
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
 #pragma unroll
-    for (int t = 0; t < kStages - 1; ++t) issue(t);
+    for (int t = 0; t < kStages - 1; ++t) issue((uint32_t)t);
 
-    uint32_t scA[4], scB[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        scA[i] = load_scale_word(sa_row[i]);
-        scB[i] = load_scale_word(sb_row[i]);
-    }
-
-    for (int64_t kt = 0; kt < nk; ++kt) {
-        // tile kt has landed once at most (kStages - 2) later groups are in flight
+    for (uint32_t kt = 0; kt < nk; ++kt) {
+        // K-tile kt has landed once at most kStages - 2 later groups are in flight
         wait_vmcnt<(kStages - 2) * kDmaPerTile>();
         block_barrier();
-        issue(kt + kStages - 1);          // refills the stage consumed in iteration kt - 1
-        uint32_t nA[4], nB[4];
-        const int64_t kn = kt + 1 < nk ? kt + 1 : kt;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            nA[i] = load_scale_word(sa_row[i] + kn * 4);
-            nB[i] = load_scale_word(sb_row[i] + kn * 4);
-        }
-        const uint8_t *As = smem[kt % kStages][0];
-        const uint8_t *Bs = smem[kt % kStages][1];
+        issue(kt + kStages - 1);           // refills the stage read in iteration kt - 1
+        const uint8_t *st = smem + (kt % kStages) * kStageBytes;
+        const uint4 wA = *reinterpret_cast<const uint4 *>(st + 2 * kCodeBytes + wave * 256);
+        const uint4 wB = *reinterpret_cast<const uint4 *>(st + 2 * kCodeBytes + wave * 256 + 16);
+        const uint32_t scA[4] = {wA.x, wA.y, wA.z, wA.w};
+        const uint32_t scB[4] = {wB.x, wB.y, wB.z, wB.w};
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
             const int cofs = ((2 * ks + half) ^ sw) * 16;
@@ -359,10 +408,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArg
             int sa[4], sb[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const uint4 qa = *reinterpret_cast<const uint4 *>(As + rd_a + i * 32 * RB + cofs);
+                const uint4 qa = *reinterpret_cast<const uint4 *>(st + rd_a + i * 32 * RB + cofs);
                 af[i][0] = (int)qa.x; af[i][1] = (int)qa.y; af[i][2] = (int)qa.z; af[i][3] = (int)qa.w;
                 af[i][4] = 0; af[i][5] = 0; af[i][6] = 0; af[i][7] = 0;
-                const uint4 qb = *reinterpret_cast<const uint4 *>(Bs + rd_b + i * 32 * RB + cofs);
+                const uint4 qb = *reinterpret_cast<const uint4 *>(st + rd_b + i * 32 * RB + cofs);
                 bf[i][0] = (int)qb.x; bf[i][1] = (int)qb.y; bf[i][2] = (int)qb.z; bf[i][3] = (int)qb.w;
                 bf[i][4] = 0; bf[i][5] = 0; bf[i][6] = 0; bf[i][7] = 0;
                 sa[i] = (int)((scA[i] >> kg8) & 0xFFu);
@@ -375,40 +424,28 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArg
                     acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
                         af[i], bf[j], acc[i][j], F::kCbsz, F::kCbsz, 0, sa[i], 0, sb[j]);
         }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) { scA[i] = nA[i]; scB[i] = nB[i]; }
     }
     wait_vmcnt<0>();
 
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t col = n0 + wn * 128 + j * 32 + (lane & 31);
-            if (col >= g.N) continue;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-                if (row >= g.M) continue;
-                float v = acc[i][j][r];
-                if (BF16OUT) {
-                    uint16_t *p = reinterpret_cast<uint16_t *>(g.c) + row * g.ldc + col;
-                    if (g.accumulate) v += bf16_to_f(*p);
-                    *p = f_to_bf16_rne(v);
-                } else {
-                    float *p = reinterpret_cast<float *>(g.c) + row * g.ldc + col;
-                    if (g.accumulate) v += *p;
-                    *p = v;
-                }
-            }
-        }
+    // ---- epilogue.  Lane holds column (lane % 32) of each 32-column tile j and
+    // rows 8 (r / 4) + 4 (lane / 32) + r % 4 of each 32-row tile i.
+    const int64_t row0 = m0 + wm * 128 + 4 * half;
+    const int64_t col0 = n0 + wn * 128 + (lane & 31);
+    if (m0 + BM2 <= g.M && n0 + BN2 <= g.N) {
+        store_tile<BF16OUT, ACC, false>(acc, g, row0, col0);
+    } else {
+        store_tile<BF16OUT, ACC, true>(acc, g, row0, col0);
+    }
 }
 
 template <bool BF>
 hipError_t launch_256(const GemmArgs &g, hipStream_t s)
 {
-    const int64_t tm = (g.M + BM2 - 1) / BM2, tn = (g.N + BN2 - 1) / BN2;
-    hipLaunchKernelGGL((gemm_fp4_256_kernel<BF>), dim3((unsigned)(tm * tn)), dim3(kThreads), 0, s, g, tm, tn);
+    const int tm = (int)((g.M + BM2 - 1) / BM2), tn = (int)((g.N + BN2 - 1) / BN2);
+    if (g.accumulate)
+        hipLaunchKernelGGL((gemm_fp4_256_kernel<BF, true>), dim3((unsigned)(tm * tn)), dim3(kThreads), 0, s, g, tm, tn);
+    else
+        hipLaunchKernelGGL((gemm_fp4_256_kernel<BF, false>), dim3((unsigned)(tm * tn)), dim3(kThreads), 0, s, g, tm, tn);
     return hipGetLastError();
 }
 
