@@ -1,6 +1,6 @@
 // C ABI of libq2d: argument validation, layout arithmetic and launches on the
 // caller's stream.  No allocation, no synchronization, no printing.
-#include "../../include/q2d.h"
+#include "q2d.h"
 #include "kernels.hpp"
 
 #include <stdint.h>

@@ -361,19 +361,6 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArg
         }
     }
     const uint32_t lds0 = (uint32_t)(uintptr_t)&smem[0];
-    // K-tile t into stage t % kStages; past the last K-tile re-read the last one
-    auto issue = [&](uint32_t t) {
-        const uint32_t tt = t < nk ? t : nk - 1;
-        const uint32_t stage = lds0 + (t % kStages) * kStageBytes;
-        const uint8_t *ba = g.a + tt * RB;
-        const uint8_t *bb = g.b + tt * RB;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            lds_dma16(ba, offA[j], stage + (4 * j + wave) * 1024);
-            lds_dma16(bb, offB[j], stage + kCodeBytes + (4 * j + wave) * 1024);
-        }
-        lds_dma4(srcS + tt * 4, stage + 2 * kCodeBytes + wave * 256);
-    };
 
     const int sw = F::swz(lane & 31);
     const int rd_a = (wm * 128 + (lane & 31)) * RB;
@@ -387,44 +374,135 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArg
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+    // operand fragments of one K-substep (64 K values): 4 A and 4 B tiles
+    uint4 fa0[4], fb0[4], fa1[4], fb1[4];
+    uint32_t scA[4], scB[4], nA[4], nB[4];
+
+    // Pipeline.  Iteration kt: (A) the 16 MFMAs of K-substep 0 of tile kt run
+    // while the fragments of substep 1 are read; (B) once tile kt+1 has landed
+    // (vmcnt + barrier; the stage of tile kt is then free because every wave
+    // holds it in registers) the 16 MFMAs of substep 1 run while the stage of
+    // tile kt is refilled with tile kt + kStages and the first substep of tile
+    // kt+1 is read.  DMA issues and LDS reads sit between MFMAs
+    // (sched_barrier pins the order) so that the texture and LDS queues never
+    // hold the wave while the matrix core starves.
+#define Q2D_MFMA(fa, fb, scA_, scB_, ks, i, j)                                                          \
+    do {                                                                                             \
+        const v8i av_ = {(int)fa[i].x, (int)fa[i].y, (int)fa[i].z, (int)fa[i].w, 0, 0, 0, 0};       \
+        const v8i bv_ = {(int)fb[j].x, (int)fb[j].y, (int)fb[j].z, (int)fb[j].w, 0, 0, 0, 0};       \
+        const int sa_ = (int)((scA_[i] >> (8 * (2 * (ks) + half))) & 0xFFu);                         \
+        const int sb_ = (int)((scB_[j] >> (8 * (2 * (ks) + half))) & 0xFFu);                         \
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av_, bv_, acc[i][j], F::kCbsz,   \
+                                                                    F::kCbsz, 0, sa_, 0, sb_);       \
+    } while (0)
+#define Q2D_READ(dstA, dstB, st, ks, i)                                                              \
+    do {                                                                                             \
+        const int cofs_ = ((2 * (ks) + half) ^ sw) * 16;                                             \
+        dstA[i] = *reinterpret_cast<const uint4 *>((st) + rd_a + (i) * 32 * RB + cofs_);            \
+        dstB[i] = *reinterpret_cast<const uint4 *>((st) + rd_b + (i) * 32 * RB + cofs_);            \
+    } while (0)
+
+    // K-tile t into stage t % kStages; past the last K-tile re-read the last one
+    auto dma_addr = [&](uint32_t t, const uint8_t *&ba, const uint8_t *&bb, const uint8_t *&bs, uint32_t &stage) {
+        const uint32_t tt = t < nk ? t : nk - 1;
+        stage = lds0 + (t % kStages) * kStageBytes;
+        ba = g.a + tt * RB;
+        bb = g.b + tt * RB;
+        bs = srcS + tt * 4;
+    };
+
+    // Each K-tile's nine loads are split: the first five (A0, B0, A1, B1, scale
+    // words) go out in phase B of the iteration that frees its stage, the last
+    // four (A2, B2, A3, B3) in phase A of the next iteration.  The prologue
+    // issues tiles 0 .. kStages-2 whole and the first part of tile kStages-1.
+    auto dma_first = [&](uint32_t t, int part) {        // part 0..4
+        const uint8_t *ba, *bb, *bs;
+        uint32_t stage;
+        dma_addr(t, ba, bb, bs, stage);
+        if (part < 4) {
+            const int jj = part >> 1;
+            if ((part & 1) == 0) lds_dma16(ba, offA[jj], stage + (4 * jj + wave) * 1024);
+            else lds_dma16(bb, offB[jj], stage + kCodeBytes + (4 * jj + wave) * 1024);
+        } else {
+            lds_dma4(bs, stage + 2 * kCodeBytes + wave * 256);
+        }
+    };
+    auto dma_second = [&](uint32_t t, int part) {       // part 0..3
+        const uint8_t *ba, *bb, *bs;
+        uint32_t stage;
+        dma_addr(t, ba, bb, bs, stage);
+        const int jj = 2 + (part >> 1);
+        if ((part & 1) == 0) lds_dma16(ba, offA[jj], stage + (4 * jj + wave) * 1024);
+        else lds_dma16(bb, offB[jj], stage + kCodeBytes + (4 * jj + wave) * 1024);
+    };
+    for (int t = 0; t < kStages; ++t) {
+        for (int p = 0; p < 5; ++p) dma_first((uint32_t)t, p);
+        if (t < kStages - 1)
+            for (int p = 0; p < 4; ++p) dma_second((uint32_t)t, p);
+    }
+    wait_vmcnt<(kStages - 2) * kDmaPerTile + 5>();
+    block_barrier();
+    {
+        const uint4 wA = *reinterpret_cast<const uint4 *>(smem + 2 * kCodeBytes + wave * 256);
+        const uint4 wB = *reinterpret_cast<const uint4 *>(smem + 2 * kCodeBytes + wave * 256 + 16);
+        scA[0] = wA.x; scA[1] = wA.y; scA[2] = wA.z; scA[3] = wA.w;
+        scB[0] = wB.x; scB[1] = wB.y; scB[2] = wB.z; scB[3] = wB.w;
 #pragma unroll
-    for (int t = 0; t < kStages - 1; ++t) issue((uint32_t)t);
+        for (int i = 0; i < 4; ++i) Q2D_READ(fa0, fb0, smem, 0, i);
+    }
 
     for (uint32_t kt = 0; kt < nk; ++kt) {
-        // K-tile kt has landed once at most kStages - 2 later groups are in flight
+        const uint8_t *st = smem + (kt % kStages) * kStageBytes;
+        // ---- phase A: substep 0 MFMAs; substep 1 reads and the last four loads
+        // of tile kt + kStages - 1 in between
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                Q2D_MFMA(fa0, fb0, scA, scB, 0, i, j);
+                __builtin_amdgcn_sched_barrier(0);
+                if (j == 1) {
+                    Q2D_READ(fa1, fb1, st, 1, i);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                if (j == 3) {
+                    dma_second(kt + kStages - 1, i);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         wait_vmcnt<(kStages - 2) * kDmaPerTile>();
         block_barrier();
-        issue(kt + kStages - 1);           // refills the stage read in iteration kt - 1
-        const uint8_t *st = smem + (kt % kStages) * kStageBytes;
-        const uint4 wA = *reinterpret_cast<const uint4 *>(st + 2 * kCodeBytes + wave * 256);
-        const uint4 wB = *reinterpret_cast<const uint4 *>(st + 2 * kCodeBytes + wave * 256 + 16);
-        const uint32_t scA[4] = {wA.x, wA.y, wA.z, wA.w};
-        const uint32_t scB[4] = {wB.x, wB.y, wB.z, wB.w};
+        // ---- phase B: substep 1 MFMAs; first five loads of tile kt + kStages
+        // into the stage of tile kt; reads of substep 0 of tile kt+1
+        const uint8_t *sn = smem + ((kt + 1) % kStages) * kStageBytes;
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const int cofs = ((2 * ks + half) ^ sw) * 16;
-            const int kg8 = 8 * (2 * ks + half);
-            v8i af[4], bf[4];
-            int sa[4], sb[4];
+        for (int i = 0; i < 4; ++i) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const uint4 qa = *reinterpret_cast<const uint4 *>(st + rd_a + i * 32 * RB + cofs);
-                af[i][0] = (int)qa.x; af[i][1] = (int)qa.y; af[i][2] = (int)qa.z; af[i][3] = (int)qa.w;
-                af[i][4] = 0; af[i][5] = 0; af[i][6] = 0; af[i][7] = 0;
-                const uint4 qb = *reinterpret_cast<const uint4 *>(st + rd_b + i * 32 * RB + cofs);
-                bf[i][0] = (int)qb.x; bf[i][1] = (int)qb.y; bf[i][2] = (int)qb.z; bf[i][3] = (int)qb.w;
-                bf[i][4] = 0; bf[i][5] = 0; bf[i][6] = 0; bf[i][7] = 0;
-                sa[i] = (int)((scA[i] >> kg8) & 0xFFu);
-                sb[i] = (int)((scB[i] >> kg8) & 0xFFu);
+            for (int j = 0; j < 4; ++j) {
+                Q2D_MFMA(fa1, fb1, scA, scB, 1, i, j);
+                __builtin_amdgcn_sched_barrier(0);
+                const int q = 4 * i + j;           // 0..15
+                if (q % 3 == 0 && q / 3 < 5) {
+                    dma_first(kt + kStages, q / 3);
+                } else if (q == 7) {
+                    const uint4 wA = *reinterpret_cast<const uint4 *>(sn + 2 * kCodeBytes + wave * 256);
+                    const uint4 wB = *reinterpret_cast<const uint4 *>(sn + 2 * kCodeBytes + wave * 256 + 16);
+                    nA[0] = wA.x; nA[1] = wA.y; nA[2] = wA.z; nA[3] = wA.w;
+                    nB[0] = wB.x; nB[1] = wB.y; nB[2] = wB.z; nB[3] = wB.w;
+                } else if (q == 8 || q == 10 || q == 11 || q == 13) {
+                    const int ii = q == 8 ? 0 : q == 10 ? 1 : q == 11 ? 2 : 3;
+                    Q2D_READ(fa0, fb0, sn, 0, ii);  // past the last tile these reads are unused
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                        af[i], bf[j], acc[i][j], F::kCbsz, F::kCbsz, 0, sa[i], 0, sb[j]);
         }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) { scA[i] = nA[i]; scB[i] = nB[i]; }
     }
+#undef Q2D_MFMA
+#undef Q2D_READ
     wait_vmcnt<0>();
 
     // ---- epilogue.  Lane holds column (lane % 32) of each 32-column tile j and
