@@ -189,6 +189,57 @@ q2d_status q2d_linear_bwd(const void *dY, q2d_dtype dt, const q2d_tensor *qX,
                           uint64_t offset_dy, q2d_tensor *qdY, void *dX, q2d_dtype dx_dt,
                           void *dW, q2d_dtype dw_dt, int accumulate_dw, hipStream_t stream);
 
+/*
+ * Grouped (mixture-of-experts) form.  The rows of x are nseg expert segments
+ * stored back to back: segment e is rows seg_offsets[e] .. seg_offsets[e+1]
+ * (seg_offsets: device array of nseg + 1 int64, ascending, seg_offsets[0] = 0,
+ * seg_offsets[nseg] = rows; 1 <= nseg <= 1024).  Each segment is its own
+ * matrix for block quantization (Sec. 3; boundary blocks over valid rows only,
+ * App. D): its 2D blocks start at its first row.  It is stored from padded row
+ * P[e] = sum over f < e of roundup(n_f, 128) of the output, so every expert's
+ * rows (codes) and every expert's K range (codes_t) start 128-aligned; padding
+ * rows and nibbles are 0.  Storage indices for the SR stream are those of x
+ * (rows counted from x), so a grouped call draws the same bits as quantizing
+ * each segment's view of the same buffer.
+ *
+ * q2d_grouped_tensor_init: layout of the padded form (rows = the capacity
+ * roundup(rows + 127 * nseg, 128), cols as given); bytes[] as q2d_tensor_init.
+ * Rows beyond the last segment's padded end are not written.  Q2D_EINVAL for
+ * rows or cols <= 0 or nseg outside [1, 1024].
+ */
+q2d_status q2d_grouped_tensor_init(q2d_tensor *t, int64_t rows, int64_t cols, int32_t nseg,
+                                   int32_t block, int64_t bytes[4]);
+
+/*
+ * Grouped 2D-block FP4 quantization of a row-major [rows, cols] x with row
+ * stride stride_r (>= cols) into `out` (from q2d_grouped_tensor_init).  Other
+ * arguments and the rounding contract as for q2d_quantize.
+ */
+q2d_status q2d_grouped_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols,
+                                int64_t stride_r, int32_t nseg, const int64_t *seg_offsets,
+                                int32_t block, q2d_round mode, uint64_t seed, uint64_t offset,
+                                q2d_tensor *out, hipStream_t stream);
+
+/*
+ * Grouped GEMMs of the expert FFN (the linear-layer GEMMs of Sec. 3 applied per
+ * expert).  total_rows = seg_offsets[nseg] (the host passes it; the offsets stay
+ * on the device).  A is a grouped tensor.
+ *  transA == 0 (ragged M; forward and data gradient): C[seg_offsets[e] + i] =
+ *    A_e[i] . op(B)_e^T for i < n_e.  op(B) is the stack of all experts'
+ *    matrices: transB == 0 takes rows [e*N, (e+1)*N) of B (B->rows = nseg*N,
+ *    N % 32 == 0, B->cols = K = A->cols); transB == 1 takes K columns
+ *    [e*K, (e+1)*K) of B^T (B->rows = nseg*K, K % 128 == 0, N = B->cols).
+ *    C is [total_rows][ldc >= N].
+ *  transA == 1 (ragged K; weight gradient), transB == 1, B grouped like A:
+ *    C_e = A_e^T . B_e (K = n_e, zero-padded to the 128-row boundary), stored at
+ *    C + e * A->cols * ldc; C is [nseg * A->cols][ldc >= B->cols].  An empty
+ *    expert gets C_e = 0 (or is left unchanged when accumulating).
+ * Q2D_EUNSUPPORTED when a code buffer the GEMM reads spans more than 4 GiB.
+ */
+q2d_status q2d_grouped_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB,
+                            int32_t nseg, const int64_t *seg_offsets, int64_t total_rows, void *C,
+                            q2d_dtype c_dt, int64_t ldc, int accumulate, hipStream_t stream);
+
 /* Static description of a status code (never NULL). */
 const char *q2d_status_string(q2d_status s);
 

@@ -16,7 +16,8 @@ import torch
 __all__ = [
     "Q2DError", "QTensor", "RTN", "SR", "FP4_2D", "MXFP8", "lib_path",
     "q2d_tensor_init", "q2d_quantize", "mxfp8_quantize", "q2d_gemm",
-    "q2d_linear_fwd", "q2d_linear_bwd", "q2d_status_string",
+    "q2d_linear_fwd", "q2d_linear_bwd", "q2d_grouped_tensor_init", "q2d_grouped_quantize",
+    "q2d_grouped_gemm", "q2d_status_string",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -53,10 +54,14 @@ def _load():
     L.q2d_gemm.argtypes = [TP, I32, TP, I32, P, I32, I64, I32, P]
     L.q2d_linear_fwd.argtypes = [P, P, I32, I64, I64, I64, I32, I32, U64, U64, U64, TP, TP, P, I32, P]
     L.q2d_linear_bwd.argtypes = [P, I32, TP, TP, I32, U64, U64, TP, P, I32, P, I32, I32, P]
+    L.q2d_grouped_tensor_init.argtypes = [TP, I64, I64, I32, I32, ctypes.POINTER(ctypes.c_int64)]
+    L.q2d_grouped_quantize.argtypes = [P, I32, I64, I64, I64, I32, P, I32, I32, U64, U64, TP, P]
+    L.q2d_grouped_gemm.argtypes = [TP, I32, TP, I32, I32, P, I64, P, I32, I64, I32, P]
     L.q2d_status_string.argtypes = [I32]
     L.q2d_status_string.restype = ctypes.c_char_p
     for name in ("q2d_tensor_init", "q2d_quantize", "mxfp8_quantize", "q2d_gemm",
-                 "q2d_linear_fwd", "q2d_linear_bwd"):
+                 "q2d_linear_fwd", "q2d_linear_bwd", "q2d_grouped_tensor_init",
+                 "q2d_grouped_quantize", "q2d_grouped_gemm"):
         getattr(L, name).restype = I32
     return L
 
@@ -89,16 +94,27 @@ class QTensor:
     """A quantized matrix in both orientations (device buffers + C descriptor).
 
     ``codes``/``scales`` hold the row-major copy, ``codes_t``/``scales_t`` the
-    transposed one; each is a 2-D uint8 tensor of shape (rows, leading dim)."""
+    transposed one; each is a 2-D uint8 tensor of shape (rows, leading dim).
+
+    With ``nseg`` set it is the padded grouped form of ``rows`` rows cut into
+    ``nseg`` segments: ``rows`` is then the padded capacity and
+    ``total_rows`` the number of input rows."""
 
     def __init__(self, fmt: int, rows: int, cols: int, device, block: int = 32,
-                 orientations=(True, True)):
+                 orientations=(True, True), nseg: int | None = None):
         self.desc = _Tensor()
         sizes = (ctypes.c_int64 * 4)()
-        _check(_lib.q2d_tensor_init(ctypes.byref(self.desc), fmt, rows, cols, block, sizes),
-               "q2d_tensor_init")
+        if nseg is None:
+            _check(_lib.q2d_tensor_init(ctypes.byref(self.desc), fmt, rows, cols, block, sizes),
+                   "q2d_tensor_init")
+        else:
+            if fmt != FP4_2D:
+                raise Q2DError("grouped tensors are 2D-block FP4 only")
+            _check(_lib.q2d_grouped_tensor_init(ctypes.byref(self.desc), rows, cols, nseg, block,
+                                                sizes), "q2d_grouped_tensor_init")
         d = self.desc
-        self.fmt, self.rows, self.cols, self.device = fmt, rows, cols, torch.device(device)
+        self.fmt, self.rows, self.cols, self.device = fmt, d.rows, cols, torch.device(device)
+        self.total_rows, self.nseg = rows, nseg
         shapes = {"codes": (sizes[0] // d.ld_codes, d.ld_codes),
                   "codes_t": (sizes[1] // d.ld_codes_t, d.ld_codes_t),
                   "scales": (sizes[2] // d.ld_scales, d.ld_scales),
@@ -205,3 +221,54 @@ def q2d_linear_bwd(dY: torch.Tensor, qX: QTensor, qW: QTensor, mode_dy="sr", see
                                _dtype_code(dW.dtype), int(bool(accumulate_dw)),
                                _stream(dY.device)), "q2d_linear_bwd")
     return dX, dW, qdY
+
+
+def q2d_grouped_tensor_init(rows: int, cols: int, nseg: int, device, block: int = 32) -> QTensor:
+    return QTensor(FP4_2D, rows, cols, device, block, nseg=nseg)
+
+
+def _check_offsets(seg_offsets: torch.Tensor, device) -> int:
+    if (not seg_offsets.is_cuda or seg_offsets.dtype != torch.int64 or seg_offsets.dim() != 1
+            or not seg_offsets.is_contiguous() or seg_offsets.device != torch.device(device)):
+        raise Q2DError("seg_offsets must be a contiguous int64 device tensor of nseg + 1 entries")
+    return seg_offsets.numel() - 1
+
+
+def q2d_grouped_quantize(x: torch.Tensor, seg_offsets: torch.Tensor, mode="rtn", seed: int = 0,
+                         offset: int = 0, out: QTensor | None = None, block: int = 32) -> QTensor:
+    """Per-expert 2D-block FP4 quantization of the expert segments of ``x`` (rows
+    seg_offsets[e] .. seg_offsets[e+1]) into the padded grouped layouts."""
+    _check_input(x)
+    if x.stride(1) != 1:
+        raise Q2DError("grouped input must have unit column stride")
+    S, C = x.shape
+    nseg = _check_offsets(seg_offsets, x.device)
+    if out is None:
+        out = QTensor(FP4_2D, S, C, x.device, block, nseg=nseg)
+    _check(_lib.q2d_grouped_quantize(x.data_ptr(), _dtype_code(x.dtype), S, C, x.stride(0), nseg,
+                                     seg_offsets.data_ptr(), block, _ROUND[mode], int(seed),
+                                     int(offset), out.ptr(), _stream(x.device)),
+           "q2d_grouped_quantize")
+    return out
+
+
+def q2d_grouped_gemm(A: QTensor, transA: int, B: QTensor, transB: int, seg_offsets: torch.Tensor,
+                     out: torch.Tensor | None = None, out_dtype=torch.float32,
+                     accumulate: bool = False) -> torch.Tensor:
+    """Per-expert GEMMs.  transA = 0: C[rows of e] = A_e op(B)_e^T over the stacked
+    expert matrices in B; transA = 1: C_e = A_e^T B_e stacked along rows."""
+    nseg = _check_offsets(seg_offsets, A.device)
+    S = A.total_rows
+    if transA:
+        shape = (nseg * A.cols, B.cols)
+    else:
+        shape = (S, B.cols if transB else B.rows // nseg)
+    if out is None:
+        out = torch.empty(shape, dtype=out_dtype, device=A.device)
+    if out.dim() != 2 or out.stride(1) != 1 or tuple(out.shape) != shape:
+        raise Q2DError("output must be a row-major %s tensor" % (shape,))
+    _check(_lib.q2d_grouped_gemm(A.ptr(), int(transA), B.ptr(), int(transB), nseg,
+                                 seg_offsets.data_ptr(), S, out.data_ptr(), _dtype_code(out.dtype),
+                                 out.stride(0), int(bool(accumulate)), _stream(A.device)),
+           "q2d_grouped_gemm")
+    return out

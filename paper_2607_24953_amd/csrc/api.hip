@@ -92,8 +92,17 @@ QuantArgs make_quant_args(const void *x, int64_t R, int64_t C, int64_t sr, int64
     a.cols_pad = rup(a.cols, 128);
     a.nbr = cdiv(a.rows, 32);
     a.nbc = cdiv(a.cols, 32);
+    a.seg_offsets = nullptr;
+    a.nseg = 0;
+    a.store_rows = a.rows;
     return a;
 }
+
+// Padded row capacity of a grouped tensor: every segment starts on a 128-row
+// boundary, so sum_e roundup(n_e, 128) <= rows + 127 * nseg.
+int64_t grouped_capacity(int64_t rows, int32_t nseg) { return rup(rows + 127 * (int64_t)nseg, 128); }
+
+constexpr int32_t kMaxGroups = 1024;
 
 q2d_status check_input(const void *x, q2d_dtype dt, int64_t R, int64_t C, int64_t sr, int64_t sc)
 {
@@ -160,6 +169,7 @@ q2d_status mxfp8_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t col
     a.scales_t = out->scales_t; a.ld_scales_t = out->ld_scales_t;
     a.rows_pad = rup(rows, 128); a.cols_pad = rup(cols, 128);
     a.nbr = rows; a.nbc = cols;
+    a.seg_offsets = nullptr; a.nseg = 0; a.store_rows = rows;
     if (launch_mxfp8_quantize(a, dtype_bytes(dt), stream) != hipSuccess) return Q2D_ELAUNCH;
     return Q2D_OK;
 }
@@ -234,6 +244,108 @@ q2d_status q2d_linear_bwd(const void *dY, q2d_dtype dt, const q2d_tensor *qX, co
     s = q2d_gemm(qdY, 0, qW, 1, dX, dx_dt, K, 0, stream);
     if (s != Q2D_OK) return s;
     return q2d_gemm(qdY, 1, qX, 1, dW, dw_dt, K, accumulate_dw, stream);
+}
+
+q2d_status q2d_grouped_tensor_init(q2d_tensor *t, int64_t rows, int64_t cols, int32_t nseg, int32_t block,
+                                   int64_t bytes[4])
+{
+    if (nseg <= 0 || nseg > kMaxGroups || rows <= 0) return Q2D_EINVAL;
+    return q2d_tensor_init(t, Q2D_FMT_FP4_2D, grouped_capacity(rows, nseg), cols, block, bytes);
+}
+
+q2d_status q2d_grouped_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols, int64_t stride_r,
+                                int32_t nseg, const int64_t *seg_offsets, int32_t block, q2d_round mode,
+                                uint64_t seed, uint64_t offset, q2d_tensor *out, hipStream_t stream)
+{
+    if (!seg_offsets || nseg <= 0 || nseg > kMaxGroups) return Q2D_EINVAL;
+    if (!aligned(seg_offsets, 8)) return Q2D_EINVAL;
+    q2d_status s = check_input(x, dt, rows > 0 ? rows : 1, cols, stride_r, 1);
+    if (s != Q2D_OK) return s;
+    if (rows <= 0 || stride_r < cols) return Q2D_EINVAL;
+    if (mode != Q2D_RTN && mode != Q2D_SR) return Q2D_EINVAL;
+    if (block != 32) return Q2D_EUNSUPPORTED;
+    const int64_t cap = grouped_capacity(rows, nseg);
+    s = check_tensor(out, Q2D_FMT_FP4_2D, cap, cols);
+    if (s != Q2D_OK) return s;
+    QuantArgs a = make_quant_args(x, rows, cols, stride_r, 1, seed, offset, out);
+    a.rows_pad = cap;               // grid bound over padded rows
+    a.seg_offsets = seg_offsets;
+    a.nseg = nseg;
+    if (launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, stream) != hipSuccess) return Q2D_ELAUNCH;
+    return Q2D_OK;
+}
+
+q2d_status q2d_grouped_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, int32_t nseg,
+                            const int64_t *seg_offsets, int64_t total_rows, void *C, q2d_dtype c_dt,
+                            int64_t ldc, int accumulate, hipStream_t stream)
+{
+    if (!A || !B || !C || !seg_offsets || !valid_dtype(c_dt)) return Q2D_EINVAL;
+    if (nseg <= 0 || nseg > kMaxGroups || total_rows <= 0 || !aligned(seg_offsets, 8)) return Q2D_EINVAL;
+    if ((transA != 0 && transA != 1) || (transB != 0 && transB != 1)) return Q2D_EINVAL;
+    if (accumulate != 0 && accumulate != 1) return Q2D_EINVAL;
+    if (A->fmt != Q2D_FMT_FP4_2D || B->fmt != Q2D_FMT_FP4_2D) return Q2D_EUNSUPPORTED;
+    if (A->block != 32 || B->block != 32) return Q2D_EUNSUPPORTED;
+    if (!aligned(C, (uintptr_t)dtype_bytes(c_dt))) return Q2D_EINVAL;
+    const int64_t cap = grouped_capacity(total_rows, nseg);
+    const Layout la = layout_of(Q2D_FMT_FP4_2D, A->rows, A->cols), lb = layout_of(Q2D_FMT_FP4_2D, B->rows, B->cols);
+    GemmArgs g;
+    GroupedArgs gr;
+    gr.seg_offsets = seg_offsets;
+    gr.nseg = nseg;
+    gr.total_rows = total_rows;
+    gr.b_group_rows = 0;
+    gr.b_group_k = 0;
+    if (A->rows != cap) return Q2D_EINVAL;
+    if (!transA) {
+        // ragged M: grouped A rows times expert e's slice of the stacked op(B)
+        gr.ragged_k = 0;
+        if (!A->codes || !check_pair(A->codes, A->ld_codes, la.ld_codes, A->scales, A->ld_scales, la.ld_scales))
+            return Q2D_EINVAL;
+        const int64_t K = A->cols;
+        int64_t N;
+        if (!transB) {
+            if (B->cols != K || B->rows % nseg != 0) return Q2D_EINVAL;
+            N = B->rows / nseg;
+            if (N % 32 != 0) return Q2D_EUNSUPPORTED;
+            if (!B->codes || !check_pair(B->codes, B->ld_codes, lb.ld_codes, B->scales, B->ld_scales, lb.ld_scales))
+                return Q2D_EINVAL;
+            g.b = B->codes; g.ldb = B->ld_codes; g.sb = B->scales; g.ldsb = B->ld_scales;
+            gr.b_group_rows = N;
+        } else {
+            if (B->rows != (int64_t)nseg * K) return Q2D_EINVAL;
+            if (K % 128 != 0) return Q2D_EUNSUPPORTED;
+            N = B->cols;
+            if (!B->codes_t ||
+                !check_pair(B->codes_t, B->ld_codes_t, lb.ld_codes_t, B->scales_t, B->ld_scales_t, lb.ld_scales_t))
+                return Q2D_EINVAL;
+            g.b = B->codes_t; g.ldb = B->ld_codes_t; g.sb = B->scales_t; g.ldsb = B->ld_scales_t;
+            gr.b_group_k = K;
+        }
+        if (ldc < N) return Q2D_EINVAL;
+        g.a = A->codes; g.lda = A->ld_codes; g.sa = A->scales; g.ldsa = A->ld_scales;
+        g.M = total_rows; g.N = N; g.K = rup(K, kPadK);
+    } else {
+        // ragged K: per-expert products of the transposed grouped operands
+        gr.ragged_k = 1;
+        if (!transB || B->rows != cap) return Q2D_EINVAL;
+        if (!A->codes_t ||
+            !check_pair(A->codes_t, A->ld_codes_t, la.ld_codes_t, A->scales_t, A->ld_scales_t, la.ld_scales_t))
+            return Q2D_EINVAL;
+        if (!B->codes_t ||
+            !check_pair(B->codes_t, B->ld_codes_t, lb.ld_codes_t, B->scales_t, B->ld_scales_t, lb.ld_scales_t))
+            return Q2D_EINVAL;
+        if (ldc < B->cols) return Q2D_EINVAL;
+        g.a = A->codes_t; g.lda = A->ld_codes_t; g.sa = A->scales_t; g.ldsa = A->ld_scales_t;
+        g.b = B->codes_t; g.ldb = B->ld_codes_t; g.sb = B->scales_t; g.ldsb = B->ld_scales_t;
+        g.M = A->cols; g.N = B->cols; g.K = 0;
+    }
+    // the grouped kernel addresses each operand with 32-bit byte offsets
+    const int64_t lim = int64_t(1) << 32;
+    if ((transA ? A->cols : A->rows) * g.lda > lim || (transB ? B->cols : B->rows) * g.ldb > lim)
+        return Q2D_EUNSUPPORTED;
+    g.c = C; g.ldc = ldc; g.accumulate = accumulate;
+    if (launch_grouped_gemm(g, gr, c_dt == Q2D_BF16, stream) != hipSuccess) return Q2D_ELAUNCH;
+    return Q2D_OK;
 }
 
 const char *q2d_status_string(q2d_status s)

@@ -113,4 +113,40 @@ __device__ __forceinline__ uint16_t f_to_bf16_rne(float f)
     return (uint16_t)(b >> 16);
 }
 
+// ---- grouped (MoE) segment tables, built per workgroup in LDS
+
+constexpr int kMaxSegs = 1024;
+
+// Inclusive prefix over `n` values produced by f(i) (i < n), written to out[1..n]
+// with out[0] = 0.  Run by one full wave; n <= kMaxSegs.
+template <typename F>
+__device__ __forceinline__ void wave_prefix(int n, F f, int32_t *out)
+{
+    const int lane = threadIdx.x & 63;
+    int32_t carry = 0;
+    if (lane == 0) out[0] = 0;
+    for (int base = 0; base < n; base += 64) {
+        const int i = base + lane;
+        int32_t v = i < n ? f(i) : 0;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int32_t u = __shfl_up(v, d);
+            if (lane >= d) v += u;
+        }
+        if (i < n) out[i + 1] = carry + v;
+        carry += __shfl(v, 63);
+    }
+}
+
+// Largest e < n with table[e] <= x (table ascending, table[0] = 0 <= x).
+__device__ __forceinline__ int seg_search(const int32_t *table, int n, int32_t x)
+{
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (table[mid] <= x) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
 }  // namespace q2d

@@ -319,16 +319,67 @@ __device__ __forceinline__ void store_tile(v16f (&acc)[4][4], const GemmArgs &g,
         }
 }
 
-template <bool BF16OUT, bool ACC>
-__global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArgs g, int tiles_m, int tiles_n)
+// GMODE 0: dense.  GMODE 1: grouped, ragged M.  GMODE 2: grouped, ragged K.
+template <bool BF16OUT, bool ACC, int GMODE>
+__global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(GemmArgs g, int tiles_m, int tiles_n,
+                                                                   const GroupedArgs gr)
 {
     using F = Fmt<kFmtFp4Block2D>;
     constexpr int RB = F::kRowBytes;                // 64
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];
 
-    int64_t tm64, tn64;
-    tile_coords(tiles_m, tiles_n, tm64, tn64);
-    const int tm = (int)tm64, tn = (int)tn64;
+    int tm, tn;
+    if (GMODE == 0) {
+        int64_t tm64, tn64;
+        tile_coords(tiles_m, tiles_n, tm64, tn64);
+        tm = (int)tm64; tn = (int)tn64;
+    } else {
+        // per-expert tables: padded start rows, and (ragged M) prefix of row tiles
+        __shared__ int32_t pad_start[kMaxSegs + 1];
+        __shared__ int32_t tile_start[kMaxSegs + 1];
+        const int64_t *off = gr.seg_offsets;
+        if ((threadIdx.x >> 6) == 0) {
+            wave_prefix(gr.nseg, [&](int i) { return (int32_t)((off[i + 1] - off[i] + 127) / 128 * 128); }, pad_start);
+            if (GMODE == 1)
+                wave_prefix(gr.nseg, [&](int i) { return (int32_t)((off[i + 1] - off[i] + BM2 - 1) / BM2); }, tile_start);
+        }
+        __syncthreads();
+        const int u = blockIdx.x;
+        int e;
+        const int esize = BF16OUT ? 2 : 4;
+        if (GMODE == 1) {
+            const int rt = u / tiles_n;
+            tn = u - rt * tiles_n;
+            if (rt >= tile_start[gr.nseg]) return;
+            e = seg_search(tile_start, gr.nseg, rt);
+            tm = rt - tile_start[e];
+            const int64_t p_e = pad_start[e];
+            g.a += p_e * g.lda;
+            g.sa += (p_e / 32) * g.ldsa;
+            g.M = off[e + 1] - off[e];
+            g.c = reinterpret_cast<uint8_t *>(g.c) + off[e] * g.ldc * esize;
+            if (gr.b_group_rows) {
+                g.b += (int64_t)e * gr.b_group_rows * g.ldb;
+                g.sb += ((int64_t)e * gr.b_group_rows / 32) * g.ldsb;
+            } else {
+                g.b += (int64_t)e * gr.b_group_k / 2;
+                g.sb += (int64_t)e * gr.b_group_k / 32;
+            }
+        } else {
+            const int per = tiles_m * tiles_n;
+            e = u / per;
+            const int rest = u - e * per;
+            tm = rest / tiles_n;
+            tn = rest - tm * tiles_n;
+            const int64_t p_e = pad_start[e];
+            g.a += p_e / 2;
+            g.sa += p_e / 32;
+            g.b += p_e / 2;
+            g.sb += p_e / 32;
+            g.K = pad_start[e + 1] - p_e;
+            g.c = reinterpret_cast<uint8_t *>(g.c) + (int64_t)e * g.M * g.ldc * esize;
+        }
+    }
     const int64_t m0 = (int64_t)tm * BM2, n0 = (int64_t)tn * BN2;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -435,6 +486,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArg
         if ((part & 1) == 0) lds_dma16(ba, offA[jj], stage + (4 * jj + wave) * 1024);
         else lds_dma16(bb, offB[jj], stage + kCodeBytes + (4 * jj + wave) * 1024);
     };
+    if (nk > 0) {
     for (int t = 0; t < kStages; ++t) {
         for (int p = 0; p < 5; ++p) dma_first((uint32_t)t, p);
         if (t < kStages - 1)
@@ -501,9 +553,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArg
 #pragma unroll
         for (int i = 0; i < 4; ++i) { scA[i] = nA[i]; scB[i] = nB[i]; }
     }
+    wait_vmcnt<0>();
+    }   // nk > 0
 #undef Q2D_MFMA
 #undef Q2D_READ
-    wait_vmcnt<0>();
 
     // ---- epilogue.  Lane holds column (lane % 32) of each 32-column tile j and
     // rows 8 (r / 4) + 4 (lane / 32) + r % 4 of each 32-row tile i.
@@ -516,14 +569,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(const GemmArg
     }
 }
 
-template <bool BF>
-hipError_t launch_256(const GemmArgs &g, hipStream_t s)
+template <bool BF, int GMODE>
+hipError_t launch_256(const GemmArgs &g, const GroupedArgs &gr, int tm, int tn, int grid, hipStream_t s)
 {
-    const int tm = (int)((g.M + BM2 - 1) / BM2), tn = (int)((g.N + BN2 - 1) / BN2);
     if (g.accumulate)
-        hipLaunchKernelGGL((gemm_fp4_256_kernel<BF, true>), dim3((unsigned)(tm * tn)), dim3(kThreads), 0, s, g, tm, tn);
+        hipLaunchKernelGGL((gemm_fp4_256_kernel<BF, true, GMODE>), dim3((unsigned)grid), dim3(kThreads), 0, s, g, tm, tn, gr);
     else
-        hipLaunchKernelGGL((gemm_fp4_256_kernel<BF, false>), dim3((unsigned)(tm * tn)), dim3(kThreads), 0, s, g, tm, tn);
+        hipLaunchKernelGGL((gemm_fp4_256_kernel<BF, false, GMODE>), dim3((unsigned)grid), dim3(kThreads), 0, s, g, tm, tn, gr);
     return hipGetLastError();
 }
 
@@ -540,11 +592,31 @@ hipError_t launch_t(const GemmArgs &g, hipStream_t s)
 hipError_t launch_gemm(const GemmArgs &g, int fmt, int c_is_bf16, hipStream_t stream)
 {
     // the 256 x 256 kernel once there are enough output tiles to fill the chip
-    if (fmt == kFmtFp4Block2D && ((g.M + BM2 - 1) / BM2) * ((g.N + BN2 - 1) / BN2) >= 128)
-        return c_is_bf16 ? launch_256<true>(g, stream) : launch_256<false>(g, stream);
+    // (its loads address each operand with 32-bit byte offsets from the K-tile base)
+    const bool off32 = g.M * g.lda <= (int64_t(1) << 32) && g.N * g.ldb <= (int64_t(1) << 32);
+    if (fmt == kFmtFp4Block2D && off32 && ((g.M + BM2 - 1) / BM2) * ((g.N + BN2 - 1) / BN2) >= 128) {
+        const int tm = (int)((g.M + BM2 - 1) / BM2), tn = (int)((g.N + BN2 - 1) / BN2);
+        const GroupedArgs none = {nullptr, 0, 0, 0, 0, 0};
+        return c_is_bf16 ? launch_256<true, 0>(g, none, tm, tn, tm * tn, stream)
+                         : launch_256<false, 0>(g, none, tm, tn, tm * tn, stream);
+    }
     if (fmt == kFmtFp4Block2D)
         return c_is_bf16 ? launch_t<kFmtFp4Block2D, true>(g, stream) : launch_t<kFmtFp4Block2D, false>(g, stream);
     return c_is_bf16 ? launch_t<kFmtMxfp8, true>(g, stream) : launch_t<kFmtMxfp8, false>(g, stream);
+}
+
+hipError_t launch_grouped_gemm(const GemmArgs &g, const GroupedArgs &gr, int c_is_bf16, hipStream_t stream)
+{
+    const int tn = (int)((g.N + BN2 - 1) / BN2);
+    if (!gr.ragged_k) {
+        // row tiles over all experts: at most total_rows / 256 + nseg
+        const int rt = (int)((gr.total_rows + BM2 - 1) / BM2) + gr.nseg;
+        return c_is_bf16 ? launch_256<true, 1>(g, gr, 0, tn, rt * tn, stream)
+                         : launch_256<false, 1>(g, gr, 0, tn, rt * tn, stream);
+    }
+    const int tm = (int)((g.M + BM2 - 1) / BM2);
+    return c_is_bf16 ? launch_256<true, 2>(g, gr, tm, tn, gr.nseg * tm * tn, stream)
+                     : launch_256<false, 2>(g, gr, tm, tn, gr.nseg * tm * tn, stream);
 }
 
 }  // namespace q2d

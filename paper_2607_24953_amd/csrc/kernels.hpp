@@ -20,6 +20,14 @@ struct QuantArgs {
     uint8_t *scales;   int64_t ld_scales;
     uint8_t *scales_t; int64_t ld_scales_t;
     int64_t nbr, nbc;              // scale-grid rows ceil(R/32) and columns ceil(C/32)
+    // Grouped (MoE) form: when seg_offsets is set, the rows are nseg segments
+    // stored back to back (segment e = rows seg_offsets[e] .. seg_offsets[e+1]);
+    // each is quantized as its own matrix and written from padded row
+    // P[e] = sum over f < e of roundup(n_f, 128).  rows_pad then bounds the
+    // padded rows and `rows` is the total number of input rows.
+    const int64_t *seg_offsets;
+    int32_t nseg;
+    int64_t store_rows;            // rows of codes / scales written (>= rows; padded rows get zeros)
 };
 
 hipError_t launch_fp4_quantize(const QuantArgs &a, int dtype_bytes, bool stochastic,
@@ -40,5 +48,21 @@ struct GemmArgs {
 enum GemmFmt { kFmtFp4Block2D = 0, kFmtMxfp8 = 1 };
 
 hipError_t launch_gemm(const GemmArgs &g, int fmt, int c_is_bf16, hipStream_t stream);
+
+// Grouped (MoE) GEMMs over nseg experts with device segment offsets.
+//   ragged M: A = grouped rows (padded), op(B) of expert e is rows
+//             [e*N, (e+1)*N) (b_group_rows = N) or K columns [e*K, (e+1)*K)
+//             (b_group_rows = 0, b_group_k = K); C rows are the unpadded rows.
+//   ragged K: A, B grouped along K (padded), C of expert e at c + e*M*ldc.
+struct GroupedArgs {
+    const int64_t *seg_offsets;
+    int32_t nseg;
+    int32_t ragged_k;
+    int64_t total_rows;        // sum of segment rows (unpadded)
+    int64_t b_group_rows;      // ragged M: rows of op(B) per expert, or 0
+    int64_t b_group_k;         // ragged M: K columns of op(B) per expert, or 0
+};
+
+hipError_t launch_grouped_gemm(const GemmArgs &g, const GroupedArgs &gr, int c_is_bf16, hipStream_t stream);
 
 }  // namespace q2d

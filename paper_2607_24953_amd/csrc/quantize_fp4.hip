@@ -9,10 +9,17 @@
 // sub-block: rows 8*(l/16) .. +7 and columns 8*(l%16) .. +7 of the strip.  A
 // row of the sub-block is one 16-byte load (bf16), so every load instruction
 // of the wave reads four 256-byte row segments.  The 8 x 8 sub-block makes the
-// transposition free: each lane packs eight nibbles per row for codes and eight
-// per column for codes_t without any data exchange.  The block maximum is a
+// transposition local: each lane packs eight nibbles per row for codes and
+// eight per column for codes_t without data exchange.  The block maximum is a
 // max over the lane's 64 values followed by four cross-lane butterflies (the 16
 // lanes of a 32 x 32 block differ in lane bits 0, 1, 4 and 5).
+//
+// Round to nearest uses gfx950's v_cvt_scalef32_pk_fp4_{bf16,f32}: it returns
+// the E2M1 code of x / S rounded to nearest even, two elements per
+// instruction, which is the round-to-nearest definition exactly (the parity
+// tests cover every bfloat16 value under every scale it can meet).
+// Stochastic rounding stays in integer/float32 ALU code because its 16 random
+// bits per element are part of the contract.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -21,6 +28,8 @@ namespace q2d {
 namespace {
 
 constexpr int kTile = 128;
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 template <typename T>
 struct Elem;
@@ -36,6 +45,12 @@ struct Elem<float> {
         out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
         out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
     }
+    // hardware round-to-nearest E2M1 pair of (lo, hi) into byte `sel` of `old`
+    template <int SEL>
+    static __device__ __forceinline__ uint32_t cvt_pair(uint32_t old, uint32_t lo, uint32_t hi, float scale)
+    {
+        return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, bits_f(lo), bits_f(hi), scale, SEL);
+    }
 };
 
 template <>
@@ -49,19 +64,79 @@ struct Elem<uint16_t> {
         out[4] = a.z << 16; out[5] = a.z & 0xFFFF0000u;
         out[6] = a.w << 16; out[7] = a.w & 0xFFFF0000u;
     }
+    template <int SEL>
+    static __device__ __forceinline__ uint32_t cvt_pair(uint32_t old, uint32_t lo, uint32_t hi, float scale)
+    {
+        // lo, hi hold bfloat16 values in their upper halves
+        const uint32_t packed = (hi & 0xFFFF0000u) | (lo >> 16);
+        return __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(old, __builtin_bit_cast(bf16x2, packed), scale, SEL);
+    }
 };
+
+// Eight elements (float32 bit patterns) -> eight nibbles, element k at bits 4k.
+template <typename T>
+__device__ __forceinline__ uint32_t cvt_row8(const uint32_t (&v)[8], float scale)
+{
+    uint32_t w = 0;
+    w = Elem<T>::template cvt_pair<0>(w, v[0], v[1], scale);
+    w = Elem<T>::template cvt_pair<1>(w, v[2], v[3], scale);
+    w = Elem<T>::template cvt_pair<2>(w, v[4], v[5], scale);
+    w = Elem<T>::template cvt_pair<3>(w, v[6], v[7], scale);
+    return w;
+}
+
+// Philox4x32-10 block with one 32x32->64 multiply per product (v_mad_u64_u32).
+__device__ __forceinline__ void philox_block(uint64_t g, uint32_t o0, uint32_t o1, uint32_t k0, uint32_t k1,
+                                             uint32_t w[4])
+{
+    uint32_t c0 = (uint32_t)g, c1 = (uint32_t)(g >> 32), c2 = o0, c3 = o1;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        c0 = n0; c1 = (uint32_t)p1; c2 = n2; c3 = (uint32_t)p0;
+    }
+    w[0] = c0; w[1] = c1; w[2] = c2; w[3] = c3;
+}
 
 // VEC: rows are read as aligned 8-element vectors (stride_c == 1).
 // SR: stochastic rounding.  ALIGNED8: every sub-block row starts at a storage
 // index that is a multiple of 8, so one Philox block serves its 8 elements.
-template <typename T, bool VEC, bool SR, bool ALIGNED8>
-__global__ __launch_bounds__(256) void fp4_quantize_kernel(const QuantArgs a)
+template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED>
+__global__ __launch_bounds__(256) void fp4_quantize_kernel(QuantArgs a)
 {
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int64_t tiles_c = a.cols_pad / kTile;
     const int64_t tile = blockIdx.x;
-    const int64_t tr = tile / tiles_c, tc = tile - tr * tiles_c;
+    int64_t tr = tile / tiles_c;
+    const int64_t tc = tile - tr * tiles_c;
+    if (GROUPED) {
+        // padded start rows of the segments; this tile's segment and its local row tile
+        __shared__ int32_t pad_start[kMaxSegs + 1];
+        const int64_t *off = a.seg_offsets;
+        if (wave == 0)
+            wave_prefix(a.nseg, [&](int i) { return (int32_t)((off[i + 1] - off[i] + 127) / 128 * 128); }, pad_start);
+        __syncthreads();
+        const int32_t prow = (int32_t)(tr * kTile);
+        if (prow >= pad_start[a.nseg]) return;
+        const int e = seg_search(pad_start, a.nseg, prow);
+        const int64_t r_begin = off[e], n_e = off[e + 1] - off[e];
+        const int32_t p_e = pad_start[e];
+        tr = (prow - p_e) / kTile;
+        a.x = reinterpret_cast<const uint8_t *>(a.x) + r_begin * a.stride_r * (int64_t)sizeof(T);
+        a.index_base += r_begin * a.stride_r;
+        a.rows = n_e;
+        a.store_rows = (n_e + 127) / 128 * 128;
+        a.nbr = a.store_rows / 32;
+        if (a.codes) a.codes += (int64_t)p_e * a.ld_codes;
+        if (a.codes_t) a.codes_t += p_e / 2;
+        if (a.scales) a.scales += (int64_t)(p_e / 32) * a.ld_scales;
+        if (a.scales_t) a.scales_t += p_e / 32;
+    }
     const int64_t strip_r = tr * kTile + wave * 32;
     const int rg = lane >> 4, cc = lane & 15;
     const int64_t r0 = strip_r + 8 * rg;
@@ -70,12 +145,22 @@ __global__ __launch_bounds__(256) void fp4_quantize_kernel(const QuantArgs a)
 
     // ---- load the 8 x 8 sub-block as float32 bit patterns (0 outside R x C)
     uint32_t v[8][8];
+    if (VEC && c0 + 8 <= a.cols) {
+        const T *xr = x + r0 * a.stride_r + c0;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int64_t r = r0 + i;
-        if (VEC && r < a.rows && c0 + 8 <= a.cols) {
-            Elem<T>::load8(x + r * a.stride_r + c0, v[i]);
-        } else {
+        for (int i = 0; i < 8; ++i) {
+            if (r0 + i < a.rows) {
+                Elem<T>::load8(xr, v[i]);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) v[i][j] = 0u;
+            }
+            xr += a.stride_r;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int64_t r = r0 + i;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int64_t c = c0 + j;
@@ -96,39 +181,42 @@ __global__ __launch_bounds__(256) void fp4_quantize_kernel(const QuantArgs a)
     am = max(am, (uint32_t)__shfl_xor((int)am, 32));
     const bool finite = am < 0x7F800000u;
     const int e = fp4_block_exponent(am);
-    const float inv = inv_pow2(e);
 
     // ---- encode
     uint32_t rowp[8], colp[8];
+    if (!SR) {
+        const float scale = bits_f((uint32_t)(127 + e) << 23);       // 2^e
 #pragma unroll
-    for (int i = 0; i < 8; ++i) { rowp[i] = 0; colp[i] = 0; }
-    const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
-    const uint32_t o0 = (uint32_t)a.offset, o1 = (uint32_t)(a.offset >> 32);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        uint32_t w[4] = {0, 0, 0, 0}, w2[4] = {0, 0, 0, 0};
-        uint64_t idx0 = 0;
-        if (SR && VEC) {
-            idx0 = (uint64_t)(a.index_base + (r0 + i) * a.stride_r + c0);
-            const uint64_t g = idx0 >> 3;
-            philox4x32_10((uint32_t)g, (uint32_t)(g >> 32), o0, o1, k0, k1, w);
-            if (!ALIGNED8) {
-                const uint64_t g2 = g + 1;
-                philox4x32_10((uint32_t)g2, (uint32_t)(g2 >> 32), o0, o1, k0, k1, w2);
-            }
-        }
+        for (int i = 0; i < 8; ++i) rowp[i] = cvt_row8<T>(v[i], scale);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const uint32_t b = v[i][j];
-            const float ax = bits_f(b & 0x7FFFFFFFu) * inv;
-            uint32_t mag;
-            if (SR) {
+            const uint32_t col[8] = {v[0][j], v[1][j], v[2][j], v[3][j], v[4][j], v[5][j], v[6][j], v[7][j]};
+            colp[j] = cvt_row8<T>(col, scale);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) { rowp[i] = 0; colp[i] = 0; }
+        const float inv = inv_pow2(e);
+        const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
+        const uint32_t o0 = (uint32_t)a.offset, o1 = (uint32_t)(a.offset >> 32);
+        int64_t idx0 = a.index_base + r0 * a.stride_r + c0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            uint32_t w[4] = {0, 0, 0, 0}, w2[4] = {0, 0, 0, 0};
+            if (VEC) {
+                philox_block((uint64_t)idx0 >> 3, o0, o1, k0, k1, w);
+                if (!ALIGNED8) philox_block(((uint64_t)idx0 >> 3) + 1, o0, o1, k0, k1, w2);
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const uint32_t b = v[i][j];
+                const float ax = bits_f(b & 0x7FFFFFFFu) * inv;
                 uint32_t r16;
                 if (VEC) {
                     if (ALIGNED8) {
                         r16 = (w[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
                     } else {
-                        const uint32_t q = (uint32_t)(idx0 & 7u) + (uint32_t)j;     // 0..14
+                        const uint32_t q = (uint32_t)(idx0 & 7) + (uint32_t)j;     // 0..14
                         const uint32_t s = q & 7u;
                         const uint32_t wa = (s & 4u) ? ((s & 2u) ? w[3] : w[2]) : ((s & 2u) ? w[1] : w[0]);
                         const uint32_t wb = (s & 4u) ? ((s & 2u) ? w2[3] : w2[2]) : ((s & 2u) ? w2[1] : w2[0]);
@@ -138,13 +226,11 @@ __global__ __launch_bounds__(256) void fp4_quantize_kernel(const QuantArgs a)
                     const uint64_t idx = (uint64_t)(a.index_base + (r0 + i) * a.stride_r + (c0 + j) * a.stride_c);
                     r16 = sr_draw(idx, k0, k1, o0, o1);
                 }
-                mag = e2m1_sr(ax, r16);
-            } else {
-                mag = e2m1_rtn(ax);
+                const uint32_t code = ((b >> 28) & 8u) | e2m1_sr(ax, r16);
+                rowp[i] |= code << (4 * j);
+                colp[j] |= code << (4 * i);
             }
-            const uint32_t code = ((b >> 28) & 8u) | mag;
-            rowp[i] |= code << (4 * j);
-            colp[j] |= code << (4 * i);
+            idx0 += a.stride_r;
         }
     }
     if (!finite) {
@@ -154,16 +240,20 @@ __global__ __launch_bounds__(256) void fp4_quantize_kernel(const QuantArgs a)
 
     // ---- stores: codes rows r < R, codes_t rows c < C, scale bytes once per block
     if (a.codes) {
+        uint8_t *dst = a.codes + r0 * a.ld_codes + (c0 >> 1);
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-            if (r0 + i < a.rows)
-                *reinterpret_cast<uint32_t *>(a.codes + (r0 + i) * a.ld_codes + (c0 >> 1)) = rowp[i];
+        for (int i = 0; i < 8; ++i) {
+            if (r0 + i < a.store_rows) *reinterpret_cast<uint32_t *>(dst) = rowp[i];
+            dst += a.ld_codes;
+        }
     }
     if (a.codes_t) {
+        uint8_t *dst = a.codes_t + c0 * a.ld_codes_t + (r0 >> 1);
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-            if (c0 + j < a.cols)
-                *reinterpret_cast<uint32_t *>(a.codes_t + (c0 + j) * a.ld_codes_t + (r0 >> 1)) = colp[j];
+        for (int j = 0; j < 8; ++j) {
+            if (c0 + j < a.cols) *reinterpret_cast<uint32_t *>(dst) = colp[j];
+            dst += a.ld_codes_t;
+        }
     }
     if (rg == 0 && (cc & 3) == 0) {
         const uint8_t sbyte = finite ? (uint8_t)(e + 127) : (uint8_t)0xFF;
@@ -173,21 +263,21 @@ __global__ __launch_bounds__(256) void fp4_quantize_kernel(const QuantArgs a)
     }
 }
 
-template <typename T, bool VEC, bool SR, bool A8>
+template <typename T, bool VEC, bool SR, bool A8, bool G>
 hipError_t launch_t(const QuantArgs &a, int64_t nblocks, hipStream_t s)
 {
-    hipLaunchKernelGGL((fp4_quantize_kernel<T, VEC, SR, A8>), dim3((unsigned)nblocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((fp4_quantize_kernel<T, VEC, SR, A8, G>), dim3((unsigned)nblocks), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
-template <typename T>
+template <typename T, bool G>
 hipError_t launch_dtype(const QuantArgs &a, bool vec, bool sr, bool a8, int64_t nb, hipStream_t s)
 {
     if (vec) {
-        if (!sr) return launch_t<T, true, false, true>(a, nb, s);
-        return a8 ? launch_t<T, true, true, true>(a, nb, s) : launch_t<T, true, true, false>(a, nb, s);
+        if (!sr) return launch_t<T, true, false, true, G>(a, nb, s);
+        return a8 ? launch_t<T, true, true, true, G>(a, nb, s) : launch_t<T, true, true, false, G>(a, nb, s);
     }
-    return sr ? launch_t<T, false, true, true>(a, nb, s) : launch_t<T, false, false, true>(a, nb, s);
+    return sr ? launch_t<T, false, true, true, G>(a, nb, s) : launch_t<T, false, false, true, G>(a, nb, s);
 }
 
 }  // namespace
@@ -198,8 +288,12 @@ hipError_t launch_fp4_quantize(const QuantArgs &a, int dtype_bytes, bool sr, hip
     const uintptr_t base = reinterpret_cast<uintptr_t>(a.x);
     const bool vec = a.stride_c == 1 && (base % 16) == 0 && ((a.stride_r * dtype_bytes) % 16) == 0;
     const bool a8 = (a.stride_r % 8) == 0 && (a.index_base % 8) == 0;
-    if (dtype_bytes == 4) return launch_dtype<float>(a, vec, sr, a8, nb, stream);
-    return launch_dtype<uint16_t>(a, vec, sr, a8, nb, stream);
+    const bool grouped = a.seg_offsets != nullptr;
+    if (dtype_bytes == 4)
+        return grouped ? launch_dtype<float, true>(a, vec, sr, a8, nb, stream)
+                       : launch_dtype<float, false>(a, vec, sr, a8, nb, stream);
+    return grouped ? launch_dtype<uint16_t, true>(a, vec, sr, a8, nb, stream)
+                   : launch_dtype<uint16_t, false>(a, vec, sr, a8, nb, stream);
 }
 
 }  // namespace q2d

@@ -29,7 +29,8 @@ def q2d():
 def test_exports_every_declared_symbol(q2d):
     names = declared_functions()
     assert {"q2d_quantize", "q2d_gemm", "mxfp8_quantize", "q2d_linear_fwd", "q2d_linear_bwd",
-            "q2d_tensor_init", "q2d_status_string"} <= set(names)
+            "q2d_tensor_init", "q2d_status_string", "q2d_grouped_tensor_init",
+            "q2d_grouped_quantize", "q2d_grouped_gemm"} <= set(names)
     lib = ctypes.CDLL(q2d.lib_path)
     for n in names:
         assert hasattr(lib, n), n
@@ -91,3 +92,76 @@ def test_error_paths(q2d):
     f.codes, f.scales, f.codes_t, f.scales_t = fake, fake, fake, fake
     assert L.q2d_gemm(ctypes.byref(d), 0, ctypes.byref(f), 0, fake, 0, 64, 0, None) == 1
     assert q2d.q2d_status_string(2) == "unsupported configuration"
+
+
+@pytest.mark.parametrize("counts,C", [([0, 1, 31, 33, 127, 130], 96), ([256], 128),
+                                      ([5] * 1024, 200), ([0, 0, 0], 32)])
+def test_grouped_layout_holds_oracle_layout(q2d, counts, C):
+    """The grouped capacity covers every padded segment the oracle lays out."""
+    import oracle
+    import synth
+    off = synth.segment_offsets(counts)
+    lay = oracle.fp4_grouped_layout(off, C)
+    P = int(oracle.grouped_rows(off)[-1])
+    S, E = int(off[-1]), len(counts)
+    d = q2d._Tensor()
+    sizes = (ctypes.c_int64 * 4)()
+    st = q2d._lib.q2d_grouped_tensor_init(ctypes.byref(d), S, C, E, 32, sizes)
+    if S == 0:
+        assert st == 1
+        return
+    assert st == 0
+    assert d.rows >= P and d.rows % 128 == 0 and d.cols == C
+    assert d.ld_codes == lay["codes"][1] and d.ld_scales == lay["scales"][1]
+    assert d.ld_codes_t >= lay["codes_t"][1] and d.ld_scales_t >= lay["scales_t"][1]
+
+
+def test_grouped_error_paths(q2d):
+    L = q2d._lib
+    sizes = (ctypes.c_int64 * 4)()
+    fake = 0x1000
+    g = q2d._Tensor()
+    assert L.q2d_grouped_tensor_init(ctypes.byref(g), 300, 64, 0, 32, sizes) == 1
+    assert L.q2d_grouped_tensor_init(ctypes.byref(g), 300, 64, 1025, 32, sizes) == 1
+    assert L.q2d_grouped_tensor_init(ctypes.byref(g), 300, 64, 4, 16, sizes) == 2
+    assert L.q2d_grouped_tensor_init(ctypes.byref(g), 300, 64, 4, 32, sizes) == 0
+    g.codes, g.scales, g.codes_t, g.scales_t = fake, fake, fake, fake
+    Q = L.q2d_grouped_quantize
+    ok = (fake, 1, 300, 64, 64, 4, fake, 32, 0, 0, 0, ctypes.byref(g), None)
+
+    def call(**kw):
+        names = ("x", "dt", "rows", "cols", "ld", "nseg", "off", "block", "mode", "seed",
+                 "offset", "out", "stream")
+        args = dict(zip(names, ok))
+        args.update(kw)
+        return Q(*[args[n] for n in names])
+
+    assert call(off=None) == 1                # no segment offsets
+    assert call(nseg=0) == 1 and call(nseg=1025) == 1
+    assert call(off=fake + 4) == 1            # misaligned offsets
+    assert call(nseg=5) == 1                  # capacity of another segment count
+    assert call(rows=400) == 1                # capacity of another row count
+    assert call(ld=32) == 1                   # row stride below cols
+    assert call(mode=7) == 1 and call(block=64) == 2
+    G = L.q2d_grouped_gemm
+    w = q2d._Tensor()
+    assert L.q2d_tensor_init(ctypes.byref(w), 0, 4 * 96, 64, 32, sizes) == 0
+    w.codes, w.scales, w.codes_t, w.scales_t = fake, fake, fake, fake
+    A, B = ctypes.byref(g), ctypes.byref(w)
+    assert G(A, 0, B, 0, 4, None, 300, fake, 0, 96, 0, None) == 1       # no offsets
+    assert G(A, 0, B, 0, 4, fake, 300, fake, 0, 95, 0, None) == 1       # ldc < N
+    assert G(A, 0, B, 0, 4, fake, 400, fake, 0, 96, 0, None) == 1       # capacity mismatch
+    w3 = q2d._Tensor()
+    assert L.q2d_tensor_init(ctypes.byref(w3), 0, 4 * 96 + 1, 64, 32, sizes) == 0
+    w3.codes, w3.scales = fake, fake
+    assert G(A, 0, ctypes.byref(w3), 0, 4, fake, 300, fake, 0, 128, 0, None) == 1  # rows % nseg
+    assert G(A, 2, B, 0, 4, fake, 300, fake, 0, 96, 0, None) == 1       # bad flag
+    assert G(A, 1, B, 0, 4, fake, 300, fake, 0, 96, 0, None) == 1       # ragged K needs transB
+    w2 = q2d._Tensor()
+    assert L.q2d_tensor_init(ctypes.byref(w2), 0, 4 * 80, 64, 32, sizes) == 0
+    w2.codes, w2.scales = fake, fake
+    assert G(A, 0, ctypes.byref(w2), 0, 4, fake, 300, fake, 0, 80, 0, None) == 2  # N % 32
+    m = q2d._Tensor()
+    assert L.q2d_tensor_init(ctypes.byref(m), 1, 4 * 96, 64, 32, sizes) == 0
+    m.codes, m.scales = fake, fake
+    assert G(A, 0, ctypes.byref(m), 0, 4, fake, 300, fake, 0, 96, 0, None) == 2   # MXFP8

@@ -14,7 +14,7 @@ import torch
 
 import oracle
 import synth
-from helpers import as_oracle_tensor, rel_frob
+from helpers import as_oracle_tensor, assert_same_bytes, gpu_buffers, rel_frob
 
 pytestmark = pytest.mark.gpu
 
@@ -29,8 +29,12 @@ def q2d():
 
 
 def quant(q2d, x, mode, seed=0, offset=0):
+    """Device quantization of x and the oracle's own quantization of the same input
+    (byte-equal; the oracle's copy feeds the float64 reference GEMM)."""
     q = q2d.q2d_quantize(x, mode, seed, offset)
-    return q, as_oracle_tensor(q, x.shape[0], x.shape[1])
+    o = oracle.quantize_fp4_2d(x.cpu(), mode, seed, offset)
+    assert_same_bytes(gpu_buffers(q), o, "operand")
+    return q, o
 
 
 def check_bf16(got, ref):
@@ -149,7 +153,7 @@ def test_gemm_mxfp8(q2d, M, N, K, ta, tb):
 
 
 def _sample_rows(qt_np, trans, rows, fmt="fp4"):
-    """float64 rows `rows` of op(X) from the host copy of a device quantization."""
+    """float64 rows `rows` of op(X) from an oracle quantization."""
     if fmt == "fp4":
         codes = qt_np["codes_t" if trans else "codes"][rows]
         scales = qt_np["scales_t" if trans else "scales"]
@@ -163,9 +167,9 @@ def _sample_rows(qt_np, trans, rows, fmt="fp4"):
 def test_full_7b_launch_configuration(q2d):
     """The benchmark's 15 GEMMs (bf16 Y and dX, fp32 dW) at full size, 48 sampled rows each.
 
-    The quantized operands are checked byte for byte against the oracle in the
-    quantizer tests; here the GEMM of the device codes is compared with the
-    float64 oracle GEMM of the same codes on sampled output rows."""
+    The oracle quantizes the same inputs (byte-equal to the device operands);
+    the device GEMMs are compared with float64 products of the oracle's
+    operands on sampled output rows."""
     w = synth.dense_7b(device=DEV)
     rng = np.random.default_rng(0)
     for lin in w.linears:
@@ -175,9 +179,11 @@ def test_full_7b_launch_configuration(q2d):
         dX, dW, qdY = q2d.q2d_linear_bwd(dY, qX, qW, w.rounding[lin.dy], seed=w.seed, offset_dy=2,
                                          dx_dtype=torch.bfloat16, dw_dtype=torch.float32)
         torch.cuda.synchronize()
-        ox = as_oracle_tensor(qX, *X.shape)
-        ow = as_oracle_tensor(qW, *W.shape)
-        ody = as_oracle_tensor(qdY, *dY.shape)
+        ox = oracle.quantize_fp4_2d(X.cpu(), w.rounding[lin.x], w.seed, 0)
+        ow = oracle.quantize_fp4_2d(W.cpu(), w.rounding[lin.w], w.seed, 1)
+        ody = oracle.quantize_fp4_2d(dY.cpu(), w.rounding[lin.dy], w.seed, 2)
+        for name, gq, oq in (("X", qX, ox), ("W", qW, ow), ("dY", qdY, ody)):
+            assert_same_bytes(gpu_buffers(gq), oq, "7B %s %s" % (lin.name, name))
         print("7B linear %s: checking sampled rows" % lin.name, flush=True)
         Wf = oracle.operand(ow, False)
         Wt = oracle.operand(ow, True)

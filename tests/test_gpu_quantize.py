@@ -113,6 +113,63 @@ def test_exhaustive_bf16_values(q2d):
         run_case(q2d, xd.t(), mode, 77, 1, "all bf16 transposed %s" % mode, x_cpu=x.t())
 
 
+def _every_value_matrix(exponents):
+    """32-row strips, one per exponent e: 32 x 32 blocks that each hold a 6 * 2^e
+    entry (so the block scale is exactly 2^e) and 1023 other finite bfloat16
+    values with |x| <= 6 * 2^e; together they list every such value once,
+    with both signs."""
+    pos = (np.arange(0x7F80, dtype=np.uint32) << 16).view(np.float32)
+    strips = []
+    for e in exponents:
+        top = np.float32(6.0 * 2.0 ** e)
+        vals = pos[pos <= top]
+        vals = np.concatenate([vals, -vals])
+        nb = -(-len(vals) // 1023)
+        blocks = np.zeros((nb, 1024), dtype=np.float32)
+        flat = blocks.reshape(-1)
+        for b in range(nb):
+            chunk = vals[b * 1023:(b + 1) * 1023]
+            blocks[b, :len(chunk)] = chunk
+            blocks[b, 1023] = top
+        strips.append(blocks.reshape(nb, 32, 32).transpose(1, 0, 2).reshape(32, nb * 32))
+    width = max(s_.shape[1] for s_ in strips)
+    out = np.zeros((32 * len(strips), width), dtype=np.float32)
+    for k, s_ in enumerate(strips):
+        out[32 * k:32 * (k + 1), :s_.shape[1]] = s_
+    return torch.from_numpy(out).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("exps", [list(range(-24, 25)), [-127, -126, -125, -100, -60, 60, 100, 124, 125]])
+def test_every_value_under_every_scale(q2d, exps):
+    """Round to nearest (and SR) of every finite bfloat16 value under each exponent it can meet."""
+    x = _every_value_matrix(exps)
+    xd = x.to(DEV)
+    for mode in ("rtn", "sr"):
+        run_case(q2d, xd, mode, 5, 6, "every value %s" % mode)
+    run_case(q2d, xd.float(), "rtn", 0, 0, "every value fp32 rtn")
+
+
+def test_fp32_midpoints_and_subnormals(q2d):
+    """float32 inputs at E2M1 midpoints +- 1 ulp and float32 subnormals, per block scale."""
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0], np.float32)
+    cand = np.concatenate([mids, np.nextafter(mids, np.float32(0)), np.nextafter(mids, np.float32(9))])
+    rows = []
+    for e in (-130, -127, -126, -20, -1, 0, 1, 7, 50, 120):
+        scale = np.float32(2.0 ** e) if e > -150 else np.float32(0)
+        blk = np.zeros(1024, np.float32)
+        blk[:len(cand)] = cand * scale
+        blk[len(cand):2 * len(cand)] = -cand * scale
+        blk[1023] = np.float32(6.0) * scale
+        rows.append(blk.reshape(32, 32))
+    sub = np.zeros(1024, np.float32)
+    sub[:512] = (np.arange(1, 513, dtype=np.uint32) * 7919).view(np.float32)     # subnormals
+    sub[512:1023] = -sub[:511]
+    rows.append(sub.reshape(32, 32))
+    x = torch.from_numpy(np.concatenate(rows, axis=1))
+    for mode in ("rtn", "sr"):
+        run_case(q2d, x.to(DEV), mode, 9, 1, "fp32 midpoints %s" % mode)
+
+
 def test_deterministic(q2d):
     x = synth.normal((512, 768), 1.0, 15, torch.bfloat16, device=DEV)
     a = gpu_buffers(q2d.q2d_quantize(x, "sr", 5, 6))
