@@ -2,10 +2,12 @@
 """Benchmark of the 2D-block FP4 linear-layer hot path on one MI355X.
 
 One step = one forward + backward pass of every linear layer of the workload:
-quantize each activation X and weight W (round to nearest) and each output
-gradient dY (stochastic rounding) once into both packed layouts, then run the
-three GEMMs of every layer, Y = X W^T (bf16 out), dX = dY W (bf16 out) and
-dW = dY^T X (fp32 out), reusing the quantized operands transposed.
+quantize each activation X and weight W and each output gradient dY once into
+both packed layouts, then run the three GEMMs of every layer, Y = X W^T (bf16
+out), dX = dY W (bf16 out) and dW = dY^T X (fp32 out), reusing the quantized
+operands transposed.  The 7B-class dense workload is the headline; the MoE
+expert FFN (grouped quantizer and grouped GEMMs) and the mixed MXFP8 / FP4 7B
+block are measured in the same run under ``other_workloads``.
 
 Prints one JSON line.  ``value`` = algorithmic GEMM flops of the step / wall
 time of the whole step (quantizers included) with all inputs resident in HBM.
@@ -13,6 +15,9 @@ The ``roofline`` object is for the dominant kernel (the FP4 GEMM), timed per
 launch with HIP events on the stream the kernels run on; ``quantizer`` reports
 the fused quantizer against the HBM roofline the same way; ``cpu_baseline`` is
 the CPU oracle timed on a bounded sample of the same workload.
+
+``--copy-calibration BYTES`` only runs a plain device copy of that size (the
+reference that scales the HBM byte counters of a profile).
 """
 from __future__ import annotations
 
@@ -36,7 +41,26 @@ WORKLOAD_TEXT = {
                 "(X, W round-to-nearest; dY stochastic), X with 1% Student-t outlier channels",
     "dense_1b": "1B-class dense MLP fwd+bwd (up 2048->5632, down 5632->2048), tokens 8192, "
                 "bf16 inputs, 32x32 2D-block FP4 with stochastic rounding on X, W and dY",
+    "moe_30b": "30B-class MoE expert FFN fwd+bwd: 16384 tokens, top-8 of 128 experts "
+               "(Zipf 1.1 routing, 131072 token slots), hidden 2048, expert FFN 768 (gate+up "
+               "2048->1536, down 768->2048); grouped 32x32 2D-block FP4 (X, W round-to-nearest; "
+               "dY stochastic)",
+    "mixed_7b": "7B-class block fwd+bwd, tokens 16384: Q/K projections in MXFP8 (E4M3, 1x32) "
+                "and V, O, gate, up, down in 32x32 2D-block FP4 with stochastic rounding; "
+                "bf16 inputs with outlier channels",
 }
+
+# what each kind of launch is measured against
+KIND_PEAK = {"gemm_fp4": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
+             "gemm_fp4_grouped": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
+             "gemm_fp8": ("mfma", PEAK_FP8_TFLOPS, "TFLOP/s"),
+             "quant_fp4": ("hbm", PEAK_HBM_GBS, "GB/s"),
+             "quant_fp4_grouped": ("hbm", PEAK_HBM_GBS, "GB/s"),
+             "quant_mxfp8": ("hbm", PEAK_HBM_GBS, "GB/s")}
+KIND_KERNEL = {"gemm_fp4": "gemm_fp4_256_kernel", "gemm_fp4_grouped": "gemm_fp4_256_kernel (grouped)",
+               "gemm_fp8": "gemm_kernel<MXFP8>", "quant_fp4": "fp4_quantize_kernel",
+               "quant_fp4_grouped": "fp4_quantize_kernel (grouped)",
+               "quant_mxfp8": "mxfp8_quantize_kernel"}
 
 
 def parse():
@@ -45,15 +69,69 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="dense_7b", choices=sorted(WORKLOAD_TEXT))
+    p.add_argument("--also", default="moe_30b,mixed_7b",
+                   help="further workloads measured in the same run (comma list, or 'none')")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-tokens", type=int, default=256)
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    p.add_argument("--summarize-profiles", default="", metavar="DIR",
+                   help="write profiles/ summaries from the rocprofv3 outputs in DIR")
     return p.parse_args()
 
 
-def quant_bytes(t) -> float:
-    """Algorithmic bytes of one quantization: input once, both 4-bit layouts, scales once."""
+def copy_calibration(torch, nbytes: int, reps: int = 3):
+    """A plain copy of nbytes (read nbytes, write nbytes) repeated `reps` times."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "reps": reps}), flush=True)
+
+
+def quant_bytes(t, fmt="fp4") -> float:
+    """Algorithmic bytes of one quantization: the input once, both code layouts, scales.
+    FP4: two 4-bit layouts and one E8M0 byte per 32x32 block; MXFP8: two 8-bit layouts
+    and one E8M0 byte per 32 elements in each layout."""
     n = t.numel()
+    if fmt == "mxfp8":
+        return n * t.element_size() + 2.0 * n + 2.0 * n / 32.0
     return n * t.element_size() + n * 0.5 * 2 + n / 1024.0
+
+
+def gemm_bytes(a_elems, b_elems, c_bytes, fmt="fp4") -> float:
+    """Algorithmic HBM bytes of one GEMM: both quantized operands once (codes and
+    scales) and the output once."""
+    if fmt == "mxfp8":
+        return (a_elems + b_elems) * (1.0 + 1.0 / 32.0) + c_bytes
+    return (a_elems + b_elems) * (0.5 + 1.0 / 1024.0) + c_bytes
+
+
+KIND_SOURCES = {"gemm_fp4": "gemm.hip", "gemm_fp4_grouped": "gemm.hip", "gemm_fp8": "gemm.hip",
+                "quant_fp4": "quantize_fp4.hip", "quant_fp4_grouped": "quantize_fp4.hip",
+                "quant_mxfp8": "quantize_mxfp8.hip"}
+
+
+def kind_hash(kind: str) -> str:
+    return source_hash(KIND_SOURCES[kind], "device_common.hpp", "kernels.hpp")
+
+
+def kind_of(kernel_name: str):
+    """Launch kind of a libq2d kernel from its (demangled) name, None for other kernels."""
+    import re
+    m = re.search(r"gemm_fp4_256_kernel<([^>]*)>", kernel_name)
+    if m:
+        return "gemm_fp4" if m.group(1).split(",")[2].strip() == "0" else "gemm_fp4_grouped"
+    m = re.search(r"gemm_kernel<(\d)", kernel_name)
+    if m:
+        return "gemm_fp4" if m.group(1) == "0" else "gemm_fp8"
+    m = re.search(r"fp4_quantize_kernel<([^>]*)>", kernel_name)
+    if m:
+        return "quant_fp4_grouped" if m.group(1).split(",")[-1].strip() == "true" else "quant_fp4"
+    if "mxfp8_quantize_kernel" in kernel_name:
+        return "quant_mxfp8"
+    return None
 
 
 def source_hash(*names) -> str:
@@ -77,56 +155,164 @@ def read_traffic(kernel: str, src_hash: str):
     return rec
 
 
+def attach_traffic(workload: str, kinds: dict):
+    """Measured HBM bytes per launch of each kind (null unless measured on these sources)."""
+    for kind, obj in kinds.items():
+        tr = read_traffic("%s/%s" % (workload, kind), kind_hash(kind))
+        obj["traffic"] = tr["bytes_per_launch"] if tr else None
+
+
 class Step:
-    """Runs one fwd+bwd pass of the workload and records per-kernel HIP events."""
+    """One fwd+bwd pass of a workload as a list of launches (kind, name, work, call);
+    work is algorithmic flops (GEMMs) or bytes (quantizers)."""
 
     def __init__(self, q2d, torch, w):
         self.q2d, self.torch, self.w = q2d, torch, w
-        dev = next(iter(w.tensors.values())).device
-        self.q = {k: q2d.QTensor(q2d.FP4_2D, t.shape[0], t.shape[1], dev) for k, t in w.tensors.items()}
-        self.out = []
+        self.dev = next(iter(w.tensors.values())).device
+        self.ops = []
+        self.events = []
+        if w.name == "moe_30b":
+            self._moe()
+        else:
+            self._dense()
+
+    def _dense(self):
+        q2d, torch, w, dev = self.q2d, self.torch, self.w, self.dev
+        qt = {}
         for lin in w.linears:
-            self.out.append((torch.empty((lin.tokens, lin.n_out), dtype=torch.bfloat16, device=dev),
-                             torch.empty((lin.tokens, lin.k_in), dtype=torch.bfloat16, device=dev),
-                             torch.empty((lin.n_out, lin.k_in), dtype=torch.float32, device=dev)))
-        self.events = None
+            for name in (lin.x, lin.w, lin.dy):
+                key = (name, lin.fmt)
+                if key in qt:
+                    continue
+                t = w.tensors[name]
+                if lin.fmt == "mxfp8":
+                    qt[key] = q2d.QTensor(q2d.MXFP8, t.shape[0], t.shape[1], dev)
+                    b = quant_bytes(t, "mxfp8")
+                    self.ops.append(("quant_mxfp8", name + ".mxfp8", b, b,
+                                     lambda t=t, o=qt[key]: q2d.mxfp8_quantize(t, out=o)))
+                else:
+                    qt[key] = q2d.QTensor(q2d.FP4_2D, t.shape[0], t.shape[1], dev)
+                    off = len(qt)
+                    b = quant_bytes(t)
+                    self.ops.append(("quant_fp4", name, b, b,
+                                     lambda t=t, o=qt[key], m=w.rounding[name], off=off:
+                                     q2d.q2d_quantize(t, m, w.seed, off, out=o)))
+        for lin in w.linears:
+            qx, qw, qdy = qt[(lin.x, lin.fmt)], qt[(lin.w, lin.fmt)], qt[(lin.dy, lin.fmt)]
+            Y = torch.empty((lin.tokens, lin.n_out), dtype=torch.bfloat16, device=dev)
+            dX = torch.empty((lin.tokens, lin.k_in), dtype=torch.bfloat16, device=dev)
+            dW = torch.empty((lin.n_out, lin.k_in), dtype=torch.float32, device=dev)
+            f = 2.0 * lin.tokens * lin.n_out * lin.k_in
+            kind = "gemm_fp8" if lin.fmt == "mxfp8" else "gemm_fp4"
+            T, N, K = lin.tokens, lin.n_out, lin.k_in
+            for nm, a, ta, b, tb, out, mnk in (("fwd", qx, 0, qw, 0, Y, (T, N, K)),
+                                               ("dX", qdy, 0, qw, 1, dX, (T, K, N)),
+                                               ("dW", qdy, 1, qx, 1, dW, (N, K, T))):
+                M_, N_, K_ = mnk
+                ab = gemm_bytes(M_ * K_, N_ * K_, out.numel() * out.element_size(), lin.fmt)
+                self.ops.append((kind, "%s.%s" % (lin.name, nm), f, ab,
+                                 lambda a=a, ta=ta, b=b, tb=tb, out=out:
+                                 q2d.q2d_gemm(a, ta, b, tb, out=out)))
+        self.flops = float(w.gemm_flops)
+
+    def _moe(self):
+        q2d, torch, w, dev = self.q2d, self.torch, self.w, self.dev
+        x = w.extra
+        off = torch.tensor(x["offsets"], dtype=torch.int64, device=dev)
+        E, S, Hd, F = x["experts"], x["slots"], x["hidden"], x["ffn"]
+        qt = {}
+        for i, name in enumerate(("X", "H", "dY_gu", "dY_d")):
+            t = w.tensors[name]
+            qt[name] = q2d.QTensor(q2d.FP4_2D, S, t.shape[1], dev, nseg=E)
+            self.ops.append(("quant_fp4_grouped", name, quant_bytes(t), quant_bytes(t),
+                             lambda t=t, o=qt[name], m=w.rounding[name], i=i:
+                             q2d.q2d_grouped_quantize(t, off, m, w.seed, i, out=o)))
+        for i, name in enumerate(("W_gu", "W_d")):
+            t = w.tensors[name]
+            qt[name] = q2d.QTensor(q2d.FP4_2D, t.shape[0], t.shape[1], dev)
+            self.ops.append(("quant_fp4", name, quant_bytes(t), quant_bytes(t),
+                             lambda t=t, o=qt[name], m=w.rounding[name], i=i:
+                             q2d.q2d_quantize(t, m, w.seed, 4 + i, out=o)))
+        bf, f32 = torch.bfloat16, torch.float32
+        gemms = [("gate_up.fwd", "X", 0, "W_gu", 0, (S, 2 * F), bf, 2.0 * S * 2 * F * Hd),
+                 ("down.fwd", "H", 0, "W_d", 0, (S, Hd), bf, 2.0 * S * Hd * F),
+                 ("down.dX", "dY_d", 0, "W_d", 1, (S, F), bf, 2.0 * S * Hd * F),
+                 ("gate_up.dX", "dY_gu", 0, "W_gu", 1, (S, Hd), bf, 2.0 * S * 2 * F * Hd),
+                 ("gate_up.dW", "dY_gu", 1, "X", 1, (E * 2 * F, Hd), f32, 2.0 * S * 2 * F * Hd),
+                 ("down.dW", "dY_d", 1, "H", 1, (E * Hd, F), f32, 2.0 * S * Hd * F)]
+        self.flops = 0.0
+        for nm, a, ta, b, tb, shape, dt, f in gemms:
+            out = torch.empty(shape, dtype=dt, device=dev)
+            ab = gemm_bytes(w.tensors[a].numel(), w.tensors[b].numel(),
+                            out.numel() * out.element_size(), "fp4")
+            self.ops.append(("gemm_fp4_grouped", nm, f, ab,
+                             lambda a=qt[a], ta=ta, b=qt[b], tb=tb, out=out:
+                             q2d.q2d_grouped_gemm(a, ta, b, tb, off, out=out)))
+            self.flops += f
+        assert abs(self.flops - x["flops"]) < 1.0
 
     def run(self, record: bool):
-        q2d, torch, w = self.q2d, self.torch, self.w
-        ev = [] if record else None
-
-        def mark(kind, work):
+        torch = self.torch
+        for kind, name, work, abytes, call in self.ops:
             if record:
                 e0 = torch.cuda.Event(enable_timing=True)
-                e0.record()
-                return (kind, work, e0)
-            return None
-
-        def done(m):
-            if m is not None:
                 e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                call()
                 e1.record()
-                ev.append(m + (e1,))
+                self.events.append((kind, name, work, abytes, e0, e1))
+            else:
+                call()
 
-        for i, (k, t) in enumerate(w.tensors.items()):
-            m = mark(("quant", k), quant_bytes(t))
-            q2d.q2d_quantize(t, w.rounding[k], w.seed, i, out=self.q[k])
-            done(m)
-        for lin, (Y, dX, dW) in zip(w.linears, self.out):
-            qx, qw, qdy = self.q[lin.x], self.q[lin.w], self.q[lin.dy]
-            f = 2.0 * lin.tokens * lin.n_out * lin.k_in
-            m = mark(("gemm", lin.name + ".fwd"), f); q2d.q2d_gemm(qx, 0, qw, 0, out=Y); done(m)
-            m = mark(("gemm", lin.name + ".dX"), f); q2d.q2d_gemm(qdy, 0, qw, 1, out=dX); done(m)
-            m = mark(("gemm", lin.name + ".dW"), f); q2d.q2d_gemm(qdy, 1, qx, 1, out=dW); done(m)
-        if record:
-            self.events = (self.events or []) + ev
+
+def measure(step, torch, steps: int, warmup: int) -> dict:
+    """Wall time of `steps` whole steps, then the same steps with HIP events around
+    every launch (on torch's current stream, the stream the launches go to)."""
+    for _ in range(warmup):
+        step.run(record=False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step.run(record=False)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step.events = []
+    for _ in range(steps):
+        step.run(record=True)
+    torch.cuda.synchronize()
+    kinds, names = {}, {}
+    for kind, name, work, abytes, e0, e1 in step.events:
+        ms = e0.elapsed_time(e1)
+        k = kinds.setdefault(kind, [0.0, 0.0, 0, 0.0])
+        k[0] += ms; k[1] += work; k[2] += 1; k[3] += abytes
+        n = names.setdefault(name, [kind, 0.0, 0.0, 0])
+        n[1] += ms; n[2] += work; n[3] += 1
+    ms_per_step = wall * 1e3 / steps
+    res = {"ms_per_step": ms_per_step, "value": step.flops / (ms_per_step * 1e-3) / 1e12,
+           "kinds": {}, "per_kernel": {}}
+    for kind, (ms, work, n, abytes) in kinds.items():
+        bound, peak, unit = KIND_PEAK[kind]
+        scale = 1e12 if unit == "TFLOP/s" else 1e9
+        ach = work / (ms * 1e-3) / scale
+        res["kinds"][kind] = {"bound": bound, "kernel": KIND_KERNEL[kind], "achieved": round(ach, 2),
+                              "peak": peak, "unit": unit, "frac": round(ach / peak, 4),
+                              "launches_timed": n, "avg_launch_ms": round(ms / n, 5),
+                              "work_per_launch": work / n, "algorithmic_bytes_per_launch": abytes / n,
+                              "ms_per_step": round(ms / steps, 4)}
+    for name, (kind, ms, work, n) in names.items():
+        unit = KIND_PEAK[kind][2]
+        rate = work / (ms * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)
+        res["per_kernel"][name] = {"ms": round(ms / n, 4), unit: round(rate, 1)}
+    return res
 
 
 def cpu_baseline(w, tokens: int):
     """The oracle (C quantizer with OpenMP, float64 numpy GEMMs) on the first `tokens`
-    rows of every activation and gradient of the workload, full weights."""
-    import numpy as np
+    rows of every activation and gradient of the workload, full weights (dense FP4
+    workloads only)."""
     import oracle
+    if not w.linears or any(l.fmt != "fp4" for l in w.linears):
+        return None
     threads = len(os.sched_getaffinity(0))
     oracle.build()
     flops = 0.0
@@ -151,13 +337,156 @@ def cpu_baseline(w, tokens: int):
                       "%.3f TFLOP" % (len(w.linears), tokens, dt, flops / 1e12)}
 
 
+PROFILE_WORKLOADS = ("dense_7b", "moe_30b", "mixed_7b")
+PROFILE_FILES = {
+    "dense_7b": [("gemm_fp4_256_kernel.dense_7b.md", ("gemm_fp4",)),
+                 ("fp4_quantize_kernel.dense_7b.md", ("quant_fp4",))],
+    "moe_30b": [("grouped_fp4_kernels.moe_30b.md", ("gemm_fp4_grouped", "quant_fp4_grouped", "quant_fp4"))],
+    "mixed_7b": [("mxfp8_kernels.mixed_7b.md", ("gemm_fp8", "quant_mxfp8", "gemm_fp4", "quant_fp4"))],
+}
+PROFILE_COMMANDS = """cd /tmp && export TMPDIR=/tmp; R=/root/repo; O=$R/gpurun_out/pb
+rocprofv3 --kernel-trace --stats --output-format csv -d $O/trace -o bench -- python3 $R/bench.py > $O/bench_trace.log 2>&1
+for c in FETCH_SIZE WRITE_SIZE; do
+  rocprofv3 --pmc $c --output-format csv -d $O/copy_$c -o copy -- python3 $R/bench.py --copy-calibration 1073741824 > $O/copy_$c.log 2>&1
+  for wl in dense_7b moe_30b mixed_7b; do
+    rocprofv3 --pmc $c --output-format csv -d $O/${wl}_$c -o $wl -- python3 $R/bench.py --workload $wl --also none --steps 1 --warmup 0 --no-cpu-baseline > $O/${wl}_$c.log 2>&1
+  done
+done
+python3 $R/bench.py --summarize-profiles $O"""
+
+
+def _json_line(path):
+    with open(path) as f:
+        for line in f:
+            if line.startswith("{"):
+                return json.loads(line)
+    raise ValueError("no JSON line in " + path)
+
+
+def _csv(dirname, suffix):
+    import csv
+    import glob
+    paths = glob.glob(os.path.join(dirname, "*" + suffix))
+    if len(paths) != 1:
+        raise ValueError("expected one *%s in %s" % (suffix, dirname))
+    with open(paths[0]) as f:
+        return list(csv.DictReader(f))
+
+
+def _counter_means(dirname, counter):
+    """Mean KiB of `counter` per dispatch for every libq2d kind (and the copy kernel)."""
+    acc = {}
+    for r in _csv(dirname, "_counter_collection.csv"):
+        if r["Counter_Name"] != counter:
+            continue
+        name = r["Kernel_Name"]
+        kind = "copy" if "copyBuffer" in name else kind_of(name)
+        if kind:
+            a = acc.setdefault(kind, [0.0, 0])
+            a[0] += float(r["Counter_Value"]); a[1] += 1
+    return {k: (v[0] / v[1], v[1]) for k, v in acc.items()}
+
+
+def summarize_profiles(d: str, out_dir: str):
+    """Turn the rocprofv3 outputs of PROFILE_COMMANDS into the text summaries of
+    `out_dir`: per-kernel duration statistics next to the benchmark's own HIP-event
+    averages, and HBM bytes per launch from FETCH_SIZE / WRITE_SIZE scaled by what
+    the same counters read for a plain copy of known size."""
+    cal = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        nbytes = _json_line(os.path.join(d, "copy_%s.log" % c))["copy_calibration_bytes"]
+        kib, n = _counter_means(os.path.join(d, "copy_" + c), c)["copy"]
+        cal[c] = {"copy_bytes": nbytes, "counter_kib": kib, "factor": nbytes / (kib * 1024.0)}
+    traffic = {"_calibration": cal}
+    for wl in PROFILE_WORKLOADS:
+        bj = _json_line(os.path.join(d, "%s_FETCH_SIZE.log" % wl))
+        fetch = _counter_means(os.path.join(d, wl + "_FETCH_SIZE"), "FETCH_SIZE")
+        write = _counter_means(os.path.join(d, wl + "_WRITE_SIZE"), "WRITE_SIZE")
+        for kind in fetch:
+            if kind == "copy" or kind not in write or kind not in bj["kinds"]:
+                continue
+            fb = fetch[kind][0] * 1024.0 * cal["FETCH_SIZE"]["factor"]
+            wb = write[kind][0] * 1024.0 * cal["WRITE_SIZE"]["factor"]
+            alg = bj["kinds"][kind]["algorithmic_bytes_per_launch"]
+            traffic["%s/%s" % (wl, kind)] = {
+                "bytes_per_launch": round(fb + wb), "fetch_bytes_per_launch": round(fb),
+                "write_bytes_per_launch": round(wb), "algorithmic_bytes_per_launch": round(alg),
+                "traffic_over_algorithmic": round((fb + wb) / alg, 3), "launches": fetch[kind][1],
+                "source_hash": bj["source_hashes"][kind]}
+    with open(os.path.join(out_dir, "traffic.json"), "w") as f:
+        json.dump(traffic, f, indent=1, sort_keys=True)
+        f.write("\n")
+
+    # kernel trace of the default benchmark run: dispatches split by workload phase
+    # (the workloads run in order; the first grouped launch starts the MoE phase and
+    # the first MXFP8 launch the mixed phase)
+    bt = _json_line(os.path.join(d, "bench_trace.log"))
+    events = {bt["config"]["name"]: bt["kinds"]}
+    for wl, o in bt.get("other_workloads", {}).items():
+        events[wl] = o["kinds"]
+    rows = _csv(os.path.join(d, "trace"), "_kernel_trace.csv")
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    phase, durs = "dense_7b", {}
+    for r in rows:
+        kind = kind_of(r["Kernel_Name"])
+        if kind is None:
+            continue
+        if kind.endswith("grouped") and phase == "dense_7b":
+            phase = "moe_30b"
+        if kind.endswith("mxfp8") or kind == "gemm_fp8":
+            phase = "mixed_7b"
+        a = durs.setdefault((phase, kind), [0.0, 0])
+        a[0] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-6; a[1] += 1
+    stats = _csv(os.path.join(d, "trace"), "_kernel_stats.csv")
+    for wl, files in PROFILE_FILES.items():
+        for fname, kinds in files:
+            out = ["# %s: %s" % (fname[:-3], ", ".join(kinds)), "",
+                   "Workload: %s." % wl, "", "Commands (rocprofv3, ROCm 7.2, one MI355X):", "",
+                   "```", PROFILE_COMMANDS, "```", "",
+                   "## Kernel duration: rocprofv3 kernel trace vs the benchmark's HIP events", "",
+                   "| kind | launches (trace, this workload) | avg ms (trace) | avg ms (HIP events) | achieved | frac of peak |",
+                   "|---|---|---|---|---|---|"]
+            for kind in kinds:
+                ms, n = durs.get((wl, kind), (0.0, 0))
+                ev = events.get(wl, {}).get(kind)
+                if not n or not ev:
+                    continue
+                out.append("| %s | %d | %.4f | %.4f | %.1f %s | %.3f |" % (
+                    kind, n, ms / n, ev["avg_launch_ms"], ev["achieved"], ev["unit"], ev["frac"]))
+            out += ["", "## HBM traffic per launch (FETCH_SIZE x %.3f + WRITE_SIZE x %.3f, copy-calibrated)"
+                    % (cal["FETCH_SIZE"]["factor"], cal["WRITE_SIZE"]["factor"]), "",
+                    "| kind | measured bytes | algorithmic bytes | ratio |", "|---|---|---|---|"]
+            for kind in kinds:
+                t = traffic.get("%s/%s" % (wl, kind))
+                if t:
+                    out.append("| %s | %d | %d | %.3f |" % (kind, t["bytes_per_launch"],
+                                                         t["algorithmic_bytes_per_launch"],
+                                                         t["traffic_over_algorithmic"]))
+            out += ["", "## rocprofv3 --stats rows of these kernels (whole benchmark run, all workloads)", "",
+                    "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
+            for r in stats:
+                if kind_of(r["Name"]) in kinds:
+                    nm = r["Name"].replace("void q2d::(anonymous namespace)::", "").split("(")[0]
+                    out.append("| %s | %s | %.1f | %.1f | %.1f |" % (
+                        nm, r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
+                        float(r["MaxNs"]) / 1e3))
+            with open(os.path.join(out_dir, fname), "w") as f:
+                f.write("\n".join(out) + "\n")
+
+
 def main():
     args = parse()
+    if args.summarize_profiles:
+        summarize_profiles(args.summarize_profiles, os.path.join(HERE, "profiles"))
+        return
     if args.gpus != 1:
         print("bench.py: this build measures one GPU only; --gpus %d is not supported" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
     import torch
+    if args.copy_calibration:
+        copy_calibration(torch, args.copy_calibration)
+        return
     import synth
     import paper_2607_24953_amd as q2d
 
@@ -165,79 +494,61 @@ def main():
     torch.cuda.set_device(dev)
     w = synth.WORKLOADS[args.workload](device=dev)
     step = Step(q2d, torch, w)
-    for _ in range(args.warmup):
-        step.run(record=False)
-    torch.cuda.synchronize()
+    res = measure(step, torch, args.steps, args.warmup)
+    print("bench: %s measured" % args.workload, file=sys.stderr, flush=True)
+    kinds = res["kinds"]
+    gemm_kind = max((k for k in kinds if k.startswith("gemm")), key=lambda k: kinds[k]["ms_per_step"])
+    quant_kind = max((k for k in kinds if k.startswith("quant")), key=lambda k: kinds[k]["ms_per_step"])
 
-    # timed region 1: wall clock of K whole steps
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step.run(record=False)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = wall * 1e3 / args.steps
-
-    # timed region 2: the same K steps with HIP events around every launch
-    for _ in range(args.steps):
-        step.run(record=True)
-    torch.cuda.synchronize()
-    t_gemm = t_quant = 0.0
-    f_gemm = b_quant = 0.0
-    n_gemm = 0
-    detail = {}
-    for (kind, name), work, e0, e1 in step.events:
-        ms = e0.elapsed_time(e1)
-        d = detail.setdefault(name, [0.0, 0.0, 0])
-        d[0] += ms; d[1] += work; d[2] += 1
-        if kind == "gemm":
-            t_gemm += ms; f_gemm += work; n_gemm += 1
-        else:
-            t_quant += ms; b_quant += work
-    per_kernel = {}
-    for name, (ms, work, n) in detail.items():
-        rate = work / (ms * 1e-3) / (1e12 if "." in name else 1e9)
-        per_kernel[name] = {"ms": round(ms / n, 4), ("TFLOP/s" if "." in name else "GB/s"): round(rate, 1)}
-    gemm_tflops = f_gemm / (t_gemm * 1e-3) / 1e12
-    quant_gbs = b_quant / (t_quant * 1e-3) / 1e9
-    flops_step = float(w.gemm_flops)
-    value = flops_step / (ms_per_step * 1e-3) / 1e12
-
-    gemm_hash = source_hash("gemm.hip", "device_common.hpp")
-    quant_hash = source_hash("quantize_fp4.hip", "device_common.hpp")
-    tr_g = read_traffic("gemm_fp4", gemm_hash)
-    tr_q = read_traffic("quantize_fp4", quant_hash)
+    attach_traffic(args.workload, kinds)
+    roof = dict(kinds[gemm_kind])
+    quant = dict(kinds[quant_kind])
 
     rec = {
         "metric": "FP4 fwd+bwd linear TFLOP/s (7B shapes) + quantizer GB/s, % of roofline",
-        "value": round(value, 2),
+        "value": round(res["value"], 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": round(res["ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "fp4_e2m1 (fp32 accumulate)",
+        "dtype": "fp4_e2m1 (fp32 accumulate)" if args.workload != "mixed_7b"
+                 else "fp4_e2m1 + fp8_e4m3 (fp32 accumulate)",
         "data": "synthetic (seeded normals, bf16; no datasets or trained weights)",
         "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload,
-                   "tokens": w.linears[0].tokens, "linears": len(w.linears),
-                   "gemms_per_step": 3 * len(w.linears), "gemm_tflop_per_step": flops_step / 1e12,
-                   "quantizations_per_step": len(w.tensors), "block": 32},
-        "roofline": {"bound": "mfma", "kernel": "gemm_kernel<FP4>", "achieved": round(gemm_tflops, 2),
-                     "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(gemm_tflops / PEAK_FP4_TFLOPS, 4),
-                     "traffic": tr_g["bytes_per_launch"] if tr_g else None,
-                     "launches_timed": n_gemm, "avg_launch_ms": round(t_gemm / max(n_gemm, 1), 5)},
-        "quantizer": {"bound": "hbm", "kernel": "fp4_quantize_kernel", "achieved": round(quant_gbs, 1),
-                      "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(quant_gbs / PEAK_HBM_GBS, 4),
-                      "traffic": tr_q["bytes_per_launch"] if tr_q else None,
-                      "ms_per_step": round(t_quant / args.steps, 4)},
-        "gemm_ms_per_step": round(t_gemm / args.steps, 4),
-        "per_kernel": per_kernel,
+                   "gemms_per_step": sum(1 for o in step.ops if o[0].startswith("gemm")),
+                   "gemm_tflop_per_step": step.flops / 1e12,
+                   "quantizations_per_step": sum(1 for o in step.ops if o[0].startswith("quant")),
+                   "block": 32},
+        "roofline": roof,
+        "quantizer": quant,
+        "kinds": kinds,
+        "per_kernel": res["per_kernel"],
+        "source_hashes": {k: kind_hash(k) for k in kinds},
     }
+    others = [a for a in args.also.split(",") if a and a != "none" and a != args.workload]
+    if others:
+        del step, w
+        torch.cuda.empty_cache()
+        rec["other_workloads"] = {}
+        for name in others:
+            wo = synth.WORKLOADS[name](device=dev)
+            so = Step(q2d, torch, wo)
+            ro = measure(so, torch, args.steps, args.warmup)
+            print("bench: %s measured" % name, file=sys.stderr, flush=True)
+            attach_traffic(name, ro["kinds"])
+            rec["other_workloads"][name] = {
+                "workload": WORKLOAD_TEXT[name], "TFLOP/s": round(ro["value"], 2),
+                "ms_per_step": round(ro["ms_per_step"], 4), "gemm_tflop_per_step": so.flops / 1e12,
+                "kinds": ro["kinds"], "per_kernel": ro["per_kernel"]}
+            del so, wo
+            torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_tokens)
+        rec["cpu_baseline"] = cpu_baseline(synth.WORKLOADS[args.workload](device=dev),
+                                           args.cpu_sample_tokens)
     print(json.dumps(rec), flush=True)
 
 
