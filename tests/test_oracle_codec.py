@@ -11,6 +11,7 @@
   within delta * 2^-16 (exactly the input when d / delta has <= 16 fraction bits).
 * E4M3 (Sec. 3.2): against torch's float8_e4m3fn cast of the exact value.
 """
+import os
 from fractions import Fraction
 
 import numpy as np
@@ -179,3 +180,35 @@ def test_e4m3_against_torch_cast():
         ref = torch.from_numpy((v * 2.0 ** (-e)).astype(np.float32)).to(torch.float8_e4m3fn)
         ref = ref.view(torch.uint8).numpy()
         np.testing.assert_array_equal(got, ref)
+
+
+def _golden_examples():
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                        "scale_and_round_examples.txt")
+    rows = []
+    with open(path) as f:
+        for line in f:
+            line = line.split("#", 1)[0].split()
+            if line:
+                rows.append(line)
+    return rows
+
+
+def test_hand_derived_examples():
+    """Worked examples derived by hand from the scale rule (Sec. 3.1; App. D) and the
+    rounding rules (App. E); each line of the fixture states its derivation."""
+    rows = _golden_examples()
+    kinds = [r[0] for r in rows]
+    assert kinds.count("scale") >= 8 and kinds.count("rtn") >= 10 and kinds.count("sr") >= 10
+    for r in rows:
+        if r[0] == "scale":
+            M, e, byte = float(r[1]), int(r[2]), int(r[3], 16)
+            got = oracle.fp4_scale_exponent(M)
+            assert got == e, r
+            assert got + 127 == byte, r
+        elif r[0] == "rtn":
+            assert oracle.fp4_code(float(r[1]), int(r[2])) == int(r[3], 16), r
+        elif r[0] == "sr":
+            assert oracle.fp4_code(float(r[1]), int(r[2]), True, int(r[3])) == int(r[4], 16), r
+        else:
+            raise AssertionError(r)

@@ -1,6 +1,7 @@
 """Pins of the oracle's Philox4x32-10 stream (the random source of stochastic
-rounding, Sec. 3.1 and App. E) against published known answers and against
-rocRAND's independent host implementation."""
+rounding, Sec. 3.1 and App. E) against rocRAND's independent host
+implementation (compiled here from the ROCm headers), including counter and
+key carries across 2^32, and a uniformity check of the 16-bit draws."""
 import os
 import shutil
 import subprocess
@@ -11,23 +12,6 @@ import pytest
 import oracle
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-
-
-def _kat():
-    rows = []
-    with open(os.path.join(HERE, "golden", "philox4x32_10_kat.txt")) as f:
-        for line in f:
-            if line.strip() and not line.startswith("#"):
-                rows.append([int(t, 16) for t in line.split()])
-    return rows
-
-
-def test_known_answers():
-    rows = _kat()
-    assert len(rows) == 3
-    for r in rows:
-        out = oracle.philox4x32_10(r[0:4], r[4:6])
-        assert [int(v) for v in out] == r[6:10]
 
 
 @pytest.fixture(scope="module")
