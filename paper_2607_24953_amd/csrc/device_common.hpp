@@ -69,29 +69,6 @@ __device__ __forceinline__ int fp8_block_exponent(uint32_t amax_bits)
 // 2^-e as a float for e in [-127, 126].
 __device__ __forceinline__ float inv_pow2(int e) { return bits_f((uint32_t)(127 - e) << 23); }
 
-// E2M1 magnitude index of v = |x| / S in [0, 6], round to nearest, ties to even.
-// The grid spacing is 1/2 below 2, 1 on [2, 4) and 2 on [4, 6]; v * (1 / spacing)
-// is exact, so rint (ties to even) of it lands on the neighbouring grid point
-// with the even mantissa bit.
-__device__ __forceinline__ uint32_t e2m1_rtn(float v)
-{
-    const float t = v < 2.0f ? 2.0f : (v < 4.0f ? 1.0f : 0.5f);
-    const int base = v < 2.0f ? 0 : (v < 4.0f ? 2 : 4);
-    return (uint32_t)((int)__builtin_rintf(v * t) + base);
-}
-
-// Stochastic rounding: floor index k plus a carry when F + r16 >= 2^16, with
-// F = floor(2^16 * (v - G[k]) / spacing).  Every step is exact in float32.
-__device__ __forceinline__ uint32_t e2m1_sr(float v, uint32_t r16)
-{
-    const float t = v < 2.0f ? 2.0f : (v < 4.0f ? 1.0f : 0.5f);
-    const int base = v < 2.0f ? 0 : (v < 4.0f ? 2 : 4);
-    const float u = v * t;
-    const float fl = __builtin_floorf(u);
-    const uint32_t F = (uint32_t)((u - fl) * 65536.0f);
-    return (uint32_t)((int)fl + base) + ((F + r16) >> 16);
-}
-
 // E4M3FN code magnitude of v in [0, 448], round to nearest even.  Below 2^-6
 // the spacing is 2^-9 (subnormals); above it the 3-bit mantissa is rounded on
 // the float32 bit pattern.

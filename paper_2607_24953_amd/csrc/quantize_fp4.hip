@@ -4,22 +4,35 @@
 // nearest or Philox stochastic rounding, and both packed layouts (row-packed
 // codes and column-packed codes_t) plus the scale grid and its transpose.
 //
-// Work split: a workgroup of 4 waves owns a 128 x 128 tile, each wave a
-// 32 x 128 strip (four 32 x 32 blocks side by side).  Lane l owns an 8 x 8
-// sub-block: rows 8*(l/16) .. +7 and columns 8*(l%16) .. +7 of the strip.  A
-// row of the sub-block is one 16-byte load (bf16), so every load instruction
-// of the wave reads four 256-byte row segments.  The 8 x 8 sub-block makes the
-// transposition local: each lane packs eight nibbles per row for codes and
-// eight per column for codes_t without data exchange.  The block maximum is a
-// max over the lane's 64 values followed by four cross-lane butterflies (the 16
-// lanes of a 32 x 32 block differ in lane bits 0, 1, 4 and 5).
+// Work split: a workgroup owns a 128-row tile of WC x 128 columns; each wave
+// owns a 32 x 128 strip (four 32 x 32 blocks side by side).  Lane l owns an
+// 8 x 8 sub-block: rows 8*(l/16) .. +7 and columns 8*(l%16) .. +7 of the strip.
+// A row of the sub-block is one 16-byte load (bf16), so every load
+// instruction of the wave reads four 256-byte row segments.  The 8 x 8
+// sub-block makes the transposition local: each lane packs eight nibbles per
+// row for codes and eight per column for codes_t without data exchange.  The
+// block maximum is a max over the lane's 64 values followed by four cross-lane
+// butterflies (the 16 lanes of a 32 x 32 block differ in lane bits 0, 1, 4, 5).
+// bfloat16 rows stay packed two elements per register.
 //
-// Round to nearest uses gfx950's v_cvt_scalef32_pk_fp4_{bf16,f32}: it returns
-// the E2M1 code of x / S rounded to nearest even, two elements per
-// instruction, which is the round-to-nearest definition exactly (the parity
-// tests cover every bfloat16 value under every scale it can meet).
-// Stochastic rounding stays in integer/float32 ALU code because its 16 random
-// bits per element are part of the contract.
+// The packed codes go through LDS and leave as 16-byte stores: full 128-byte
+// lines of codes when the tile is 256 columns wide (WC = 2, round to nearest),
+// 64-byte runs of codes_t.
+//
+// Round to nearest uses gfx950's v_cvt_scalef32_pk_fp4_{bf16,f32}: the E2M1
+// code of x / S rounded to nearest even, two elements per instruction, which
+// is the round-to-nearest definition exactly.
+//
+// Stochastic rounding uses v_cvt_scalef32_sr_pk_fp4_f32.  It converts a pair
+// with one 32-bit seed: the first element adds seed >> 10 below its kept
+// mantissa bit (after aligning subnormal E2M1 results) and truncates, the
+// second element adds (seed << 1) >> 10.  A seed of r16 << 16 for the first
+// element, or r16 << 15 for the second, therefore rounds the magnitude up
+// exactly when floor(2^16 d / delta) + r16 >= 2^16 -- the rounding contract of
+// this library.  Each element is converted in an instruction where it has its
+// own draw; the other nibble of that result is dropped.  The parity tests
+// compare every bfloat16 value under every scale, in both modes, bit for bit
+// with the CPU definition.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -27,9 +40,10 @@ namespace q2d {
 
 namespace {
 
-constexpr int kTile = 128;
+constexpr int kTile = 128;          // tile rows
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f2v __attribute__((ext_vector_type(2)));
 
 template <typename T>
 struct Elem;
@@ -37,52 +51,36 @@ struct Elem;
 template <>
 struct Elem<float> {
     static __device__ __forceinline__ uint32_t bits(const float *p) { return f_bits(*p); }
-    // eight consecutive elements of one row, 16-byte aligned
-    static __device__ __forceinline__ void load8(const float *p, uint32_t out[8])
-    {
-        const uint4 a = *reinterpret_cast<const uint4 *>(p);
-        const uint4 b = *reinterpret_cast<const uint4 *>(p + 4);
-        out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
-        out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
-    }
-    // hardware round-to-nearest E2M1 pair of (lo, hi) into byte `sel` of `old`
-    template <int SEL>
-    static __device__ __forceinline__ uint32_t cvt_pair(uint32_t old, uint32_t lo, uint32_t hi, float scale)
-    {
-        return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, bits_f(lo), bits_f(hi), scale, SEL);
-    }
 };
 
 template <>
 struct Elem<uint16_t> {
     static __device__ __forceinline__ uint32_t bits(const uint16_t *p) { return (uint32_t)*p << 16; }
-    static __device__ __forceinline__ void load8(const uint16_t *p, uint32_t out[8])
-    {
-        const uint4 a = *reinterpret_cast<const uint4 *>(p);
-        out[0] = a.x << 16; out[1] = a.x & 0xFFFF0000u;
-        out[2] = a.y << 16; out[3] = a.y & 0xFFFF0000u;
-        out[4] = a.z << 16; out[5] = a.z & 0xFFFF0000u;
-        out[6] = a.w << 16; out[7] = a.w & 0xFFFF0000u;
-    }
-    template <int SEL>
-    static __device__ __forceinline__ uint32_t cvt_pair(uint32_t old, uint32_t lo, uint32_t hi, float scale)
-    {
-        // lo, hi hold bfloat16 values in their upper halves
-        const uint32_t packed = (hi & 0xFFFF0000u) | (lo >> 16);
-        return __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(old, __builtin_bit_cast(bf16x2, packed), scale, SEL);
-    }
 };
 
-// Eight elements (float32 bit patterns) -> eight nibbles, element k at bits 4k.
-template <typename T>
-__device__ __forceinline__ uint32_t cvt_row8(const uint32_t (&v)[8], float scale)
+// Round-to-nearest E2M1 pair into byte SEL of `old`: f32 sources as two
+// float32 bit patterns, bf16 sources as one packed register (low half first).
+template <int SEL>
+__device__ __forceinline__ uint32_t rtn_pair_f32(uint32_t old, uint32_t lo, uint32_t hi, float scale)
 {
-    uint32_t w = 0;
-    w = Elem<T>::template cvt_pair<0>(w, v[0], v[1], scale);
-    w = Elem<T>::template cvt_pair<1>(w, v[2], v[3], scale);
-    w = Elem<T>::template cvt_pair<2>(w, v[4], v[5], scale);
-    w = Elem<T>::template cvt_pair<3>(w, v[6], v[7], scale);
-    return w;
+    return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, bits_f(lo), bits_f(hi), scale, SEL);
+}
+template <int SEL>
+__device__ __forceinline__ uint32_t rtn_pair_bf16(uint32_t old, uint32_t packed, float scale)
+{
+    return __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(old, __builtin_bit_cast(bf16x2, packed), scale, SEL);
+}
+
+// Stochastic E2M1 conversion of a pair into byte `sel`; the other bytes of the
+// result are not defined and the caller masks them.
+__device__ __forceinline__ uint32_t sr_pair(int sel, f2v v, uint32_t seed, float scale)
+{
+    switch (sel) {
+    case 0: return __builtin_amdgcn_cvt_scalef32_sr_pk_fp4_f32(0u, v, seed, scale, 0);
+    case 1: return __builtin_amdgcn_cvt_scalef32_sr_pk_fp4_f32(0u, v, seed, scale, 1);
+    case 2: return __builtin_amdgcn_cvt_scalef32_sr_pk_fp4_f32(0u, v, seed, scale, 2);
+    default: return __builtin_amdgcn_cvt_scalef32_sr_pk_fp4_f32(0u, v, seed, scale, 3);
+    }
 }
 
 // Philox4x32-10 block with one 32x32->64 multiply per product (v_mad_u64_u32).
@@ -105,12 +103,19 @@ __device__ __forceinline__ void philox_block(uint64_t g, uint32_t o0, uint32_t o
 // VEC: rows are read as aligned 8-element vectors (stride_c == 1).
 // SR: stochastic rounding.  ALIGNED8: every sub-block row starts at a storage
 // index that is a multiple of 8, so one Philox block serves its 8 elements.
-template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED>
-__global__ __launch_bounds__(256) void fp4_quantize_kernel(QuantArgs a)
+// GROUPED: the rows are expert segments (see QuantArgs).  WC: 128-column
+// strips per tile (waves side by side).
+template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED, int WC>
+__global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
 {
+    constexpr int kTC = 128 * WC;
+    constexpr int kThreads = 256 * WC;
+    constexpr bool PK = sizeof(T) == 2;     // bf16: two elements per register
+    constexpr int NV = PK ? 4 : 8;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int64_t tiles_c = a.cols_pad / kTile;
+    const int wr = wave / WC, wc = wave % WC;
+    const int64_t tiles_c = (a.cols_pad + kTC - 1) / kTC;
     const int64_t tile = blockIdx.x;
     int64_t tr = tile / tiles_c;
     const int64_t tc = tile - tr * tiles_c;
@@ -137,24 +142,50 @@ __global__ __launch_bounds__(256) void fp4_quantize_kernel(QuantArgs a)
         if (a.scales) a.scales += (int64_t)(p_e / 32) * a.ld_scales;
         if (a.scales_t) a.scales_t += p_e / 32;
     }
-    const int64_t strip_r = tr * kTile + wave * 32;
+    const int64_t strip_r = tr * kTile + wr * 32;
     const int rg = lane >> 4, cc = lane & 15;
     const int64_t r0 = strip_r + 8 * rg;
-    const int64_t c0 = tc * kTile + 8 * cc;
+    const int64_t c0 = tc * kTC + wc * 128 + 8 * cc;
+    const bool col_ok = tc * kTC + wc * 128 < a.cols_pad;     // strip inside the padded width
     const T *x = reinterpret_cast<const T *>(a.x);
 
-    // ---- load the 8 x 8 sub-block as float32 bit patterns (0 outside R x C)
-    uint32_t v[8][8];
-    if (VEC && c0 + 8 <= a.cols) {
+    // ---- load the 8 x 8 sub-block (0 outside R x C).  bf16: v[i][k] holds
+    // columns 2k (low half) and 2k+1 (high half) of row i; fp32: bit patterns.
+    uint32_t v[8][NV];
+    if (PK) {
+        if (VEC && c0 + 8 <= a.cols) {
+            const T *xr = x + r0 * a.stride_r + c0;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                uint4 q = make_uint4(0u, 0u, 0u, 0u);
+                if (r0 + i < a.rows) q = *reinterpret_cast<const uint4 *>(xr);
+                v[i][0] = q.x; v[i][1] = q.y; v[i][2] = q.z; v[i][3] = q.w;
+                xr += a.stride_r;
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int64_t r = r0 + i;
+#pragma unroll
+                for (int k = 0; k < NV; ++k) {
+                    const int64_t c = c0 + 2 * k;
+                    const uint32_t lo = (r < a.rows && c < a.cols) ? Elem<T>::bits(x + r * a.stride_r + c * a.stride_c) : 0u;
+                    const uint32_t hi = (r < a.rows && c + 1 < a.cols) ? Elem<T>::bits(x + r * a.stride_r + (c + 1) * a.stride_c) : 0u;
+                    v[i][k] = (lo >> 16) | hi;
+                }
+            }
+        }
+    } else if (VEC && c0 + 8 <= a.cols) {
         const T *xr = x + r0 * a.stride_r + c0;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
+            uint4 q0 = make_uint4(0u, 0u, 0u, 0u), q1 = q0;
             if (r0 + i < a.rows) {
-                Elem<T>::load8(xr, v[i]);
-            } else {
-#pragma unroll
-                for (int j = 0; j < 8; ++j) v[i][j] = 0u;
+                q0 = *reinterpret_cast<const uint4 *>(xr);
+                q1 = *reinterpret_cast<const uint4 *>(xr + 4);
             }
+            v[i][0] = q0.x; v[i][1] = q0.y; v[i][2] = q0.z; v[i][3] = q0.w;
+            v[i][NV - 4] = q1.x; v[i][NV - 3] = q1.y; v[i][NV - 2] = q1.z; v[i][NV - 1] = q1.w;
             xr += a.stride_r;
         }
     } else {
@@ -162,75 +193,144 @@ __global__ __launch_bounds__(256) void fp4_quantize_kernel(QuantArgs a)
         for (int i = 0; i < 8; ++i) {
             const int64_t r = r0 + i;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
+            for (int j = 0; j < NV; ++j) {
                 const int64_t c = c0 + j;
                 v[i][j] = (r < a.rows && c < a.cols) ? Elem<T>::bits(x + r * a.stride_r + c * a.stride_c) : 0u;
             }
         }
     }
+    // float32 bit pattern of element (i, j)
+    auto elem = [&](int i, int j) -> uint32_t {
+        if (PK) return (j & 1) ? (v[i][j >> 1] & 0xFFFF0000u) : (v[i][j >> 1] << 16);
+        return v[i][j];
+    };
 
     // ---- block maximum on |bits| (NaN > inf > finite, as unsigned integers)
     uint32_t am = 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) am = max(am, v[i][j] & 0x7FFFFFFFu);
+        for (int k = 0; k < NV; ++k) {
+            if (PK) {
+                const uint32_t w = v[i][k] & 0x7FFF7FFFu;
+                am = max(am, max(w & 0xFFFFu, w >> 16));
+            } else {
+                am = max(am, v[i][k] & 0x7FFFFFFFu);
+            }
+        }
+    if (PK) am <<= 16;
     am = max(am, (uint32_t)__shfl_xor((int)am, 1));
     am = max(am, (uint32_t)__shfl_xor((int)am, 2));
     am = max(am, (uint32_t)__shfl_xor((int)am, 16));
     am = max(am, (uint32_t)__shfl_xor((int)am, 32));
     const bool finite = am < 0x7F800000u;
     const int e = fp4_block_exponent(am);
+    const float scale = bits_f((uint32_t)(127 + e) << 23);       // 2^e
 
-    // ---- encode
+    // ---- encode: rowp[i] = eight nibbles of row i, colp[j] = eight nibbles of column j
     uint32_t rowp[8], colp[8];
     if (!SR) {
-        const float scale = bits_f((uint32_t)(127 + e) << 23);       // 2^e
-#pragma unroll
-        for (int i = 0; i < 8; ++i) rowp[i] = cvt_row8<T>(v[i], scale);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const uint32_t col[8] = {v[0][j], v[1][j], v[2][j], v[3][j], v[4][j], v[5][j], v[6][j], v[7][j]};
-            colp[j] = cvt_row8<T>(col, scale);
-        }
-    } else {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) { rowp[i] = 0; colp[i] = 0; }
-        const float inv = inv_pow2(e);
-        const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
-        const uint32_t o0 = (uint32_t)a.offset, o1 = (uint32_t)(a.offset >> 32);
-        int64_t idx0 = a.index_base + r0 * a.stride_r + c0;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            uint32_t w[4] = {0, 0, 0, 0}, w2[4] = {0, 0, 0, 0};
-            if (VEC) {
-                philox_block((uint64_t)idx0 >> 3, o0, o1, k0, k1, w);
-                if (!ALIGNED8) philox_block(((uint64_t)idx0 >> 3) + 1, o0, o1, k0, k1, w2);
+            uint32_t w = 0;
+            if (PK) {
+                w = rtn_pair_bf16<0>(w, v[i][0], scale);
+                w = rtn_pair_bf16<1>(w, v[i][1], scale);
+                w = rtn_pair_bf16<2>(w, v[i][2], scale);
+                w = rtn_pair_bf16<3>(w, v[i][3], scale);
+            } else {
+                w = rtn_pair_f32<0>(w, elem(i, 0), elem(i, 1), scale);
+                w = rtn_pair_f32<1>(w, elem(i, 2), elem(i, 3), scale);
+                w = rtn_pair_f32<2>(w, elem(i, 4), elem(i, 5), scale);
+                w = rtn_pair_f32<3>(w, elem(i, 6), elem(i, 7), scale);
             }
+            rowp[i] = w;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            uint32_t w = 0;
+            if (PK) {
+                // rows (2m, 2m+1) of column j as one packed pair
+                const int k = j >> 1;
+                auto pr = [&](int m) -> uint32_t {
+                    const uint32_t lo = v[2 * m][k], hi = v[2 * m + 1][k];
+                    return (j & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
+                };
+                w = rtn_pair_bf16<0>(w, pr(0), scale);
+                w = rtn_pair_bf16<1>(w, pr(1), scale);
+                w = rtn_pair_bf16<2>(w, pr(2), scale);
+                w = rtn_pair_bf16<3>(w, pr(3), scale);
+            } else {
+                w = rtn_pair_f32<0>(w, elem(0, j), elem(1, j), scale);
+                w = rtn_pair_f32<1>(w, elem(2, j), elem(3, j), scale);
+                w = rtn_pair_f32<2>(w, elem(4, j), elem(5, j), scale);
+                w = rtn_pair_f32<3>(w, elem(6, j), elem(7, j), scale);
+            }
+            colp[j] = w;
+        }
+    } else {
+        const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
+        const uint32_t o0 = (uint32_t)a.offset, o1 = (uint32_t)(a.offset >> 32);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) { rowp[i] = 0; colp[i] = 0; }
+        int64_t idx0 = a.index_base + r0 * a.stride_r + c0;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            // draws of rows 2m and 2m+1 as seeds r16 << 16
+            uint32_t s16[2][8];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int i = 2 * m + h;
+                uint32_t w[4] = {0, 0, 0, 0}, w2[4] = {0, 0, 0, 0};
+                if (VEC) {
+                    philox_block((uint64_t)idx0 >> 3, o0, o1, k0, k1, w);
+                    if (!ALIGNED8) philox_block(((uint64_t)idx0 >> 3) + 1, o0, o1, k0, k1, w2);
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    uint32_t r;
+                    if (VEC) {
+                        if (ALIGNED8) {
+                            r = (j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16);
+                        } else {
+                            // the row's eight draws straddle two Philox blocks
+                            const uint32_t q = (uint32_t)(idx0 & 7) + (uint32_t)j;     // 0..14
+                            const uint32_t sq = q & 7u;
+                            const uint32_t wa = (sq & 4u) ? ((sq & 2u) ? w[3] : w[2]) : ((sq & 2u) ? w[1] : w[0]);
+                            const uint32_t wb = (sq & 4u) ? ((sq & 2u) ? w2[3] : w2[2]) : ((sq & 2u) ? w2[1] : w2[0]);
+                            const uint32_t ww = q < 8u ? wa : wb;
+                            r = (sq & 1u) ? (ww & 0xFFFF0000u) : (ww << 16);
+                        }
+                    } else {
+                        const uint64_t idx = (uint64_t)(a.index_base + (r0 + i) * a.stride_r + (c0 + j) * a.stride_c);
+                        r = sr_draw(idx, k0, k1, o0, o1) << 16;
+                    }
+                    s16[h][j] = r;
+                }
+                idx0 += a.stride_r;
+            }
+            // rows 2m and 2m+1: pairs (2k, 2k+1) into byte k
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int i = 2 * m + h;
+                uint32_t acc = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const f2v pr = {bits_f(elem(i, 2 * k)), bits_f(elem(i, 2 * k + 1))};
+                    const uint32_t lo = sr_pair(k, pr, s16[h][2 * k], scale);
+                    const uint32_t hi = sr_pair(k, pr, s16[h][2 * k + 1] >> 1, scale);
+                    acc |= (lo & (0x0Fu << (8 * k))) | (hi & (0xF0u << (8 * k)));
+                }
+                rowp[i] = acc;
+            }
+            // every column: rows (2m, 2m+1) into byte m
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                const uint32_t b = v[i][j];
-                const float ax = bits_f(b & 0x7FFFFFFFu) * inv;
-                uint32_t r16;
-                if (VEC) {
-                    if (ALIGNED8) {
-                        r16 = (w[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
-                    } else {
-                        const uint32_t q = (uint32_t)(idx0 & 7) + (uint32_t)j;     // 0..14
-                        const uint32_t s = q & 7u;
-                        const uint32_t wa = (s & 4u) ? ((s & 2u) ? w[3] : w[2]) : ((s & 2u) ? w[1] : w[0]);
-                        const uint32_t wb = (s & 4u) ? ((s & 2u) ? w2[3] : w2[2]) : ((s & 2u) ? w2[1] : w2[0]);
-                        r16 = ((q < 8u ? wa : wb) >> ((s & 1u) * 16u)) & 0xFFFFu;
-                    }
-                } else {
-                    const uint64_t idx = (uint64_t)(a.index_base + (r0 + i) * a.stride_r + (c0 + j) * a.stride_c);
-                    r16 = sr_draw(idx, k0, k1, o0, o1);
-                }
-                const uint32_t code = ((b >> 28) & 8u) | e2m1_sr(ax, r16);
-                rowp[i] |= code << (4 * j);
-                colp[j] |= code << (4 * i);
+                const f2v pr = {bits_f(elem(2 * m, j)), bits_f(elem(2 * m + 1, j))};
+                const uint32_t lo = sr_pair(m, pr, s16[0][j], scale);
+                const uint32_t hi = sr_pair(m, pr, s16[1][j] >> 1, scale);
+                colp[j] |= (lo & (0x0Fu << (8 * m))) | (hi & (0xF0u << (8 * m)));
             }
-            idx0 += a.stride_r;
         }
     }
     if (!finite) {
@@ -238,24 +338,41 @@ __global__ __launch_bounds__(256) void fp4_quantize_kernel(QuantArgs a)
         for (int i = 0; i < 8; ++i) { rowp[i] = 0; colp[i] = 0; }
     }
 
-    // ---- stores: codes rows r < R, codes_t rows c < C, scale bytes once per block
-    if (a.codes) {
-        uint8_t *dst = a.codes + r0 * a.ld_codes + (c0 >> 1);
+    // ---- stores through LDS: 16 bytes per lane, codes rows r < store_rows as
+    // WC * 64-byte runs, codes_t rows c < C as 64-byte runs
+    __shared__ uint32_t st_r[kTile][16 * WC + 1];
+    __shared__ uint32_t st_c[kTC][17];
+    {
+        const int rl = wr * 32 + 8 * rg;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            if (r0 + i < a.store_rows) *reinterpret_cast<uint32_t *>(dst) = rowp[i];
-            dst += a.ld_codes;
+        for (int i = 0; i < 8; ++i) st_r[rl + i][wc * 16 + cc] = rowp[i];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) st_c[wc * 128 + 8 * cc + j][wr * 4 + rg] = colp[j];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int item = threadIdx.x + kThreads * q;
+        if (a.codes) {
+            const int line = item / (4 * WC), part = item % (4 * WC);
+            const int64_t r = tr * kTile + line;
+            if (r < a.store_rows && tc * kTC + part * 32 < a.cols_pad) {
+                const uint4 w = make_uint4(st_r[line][4 * part], st_r[line][4 * part + 1],
+                                           st_r[line][4 * part + 2], st_r[line][4 * part + 3]);
+                *reinterpret_cast<uint4 *>(a.codes + r * a.ld_codes + tc * (kTC / 2) + part * 16) = w;
+            }
+        }
+        if (a.codes_t) {
+            const int line = item >> 2, part = item & 3;
+            const int64_t c = tc * kTC + line;
+            if (c < a.cols) {
+                const uint4 w = make_uint4(st_c[line][4 * part], st_c[line][4 * part + 1],
+                                           st_c[line][4 * part + 2], st_c[line][4 * part + 3]);
+                *reinterpret_cast<uint4 *>(a.codes_t + c * a.ld_codes_t + tr * (kTile / 2) + part * 16) = w;
+            }
         }
     }
-    if (a.codes_t) {
-        uint8_t *dst = a.codes_t + c0 * a.ld_codes_t + (r0 >> 1);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            if (c0 + j < a.cols) *reinterpret_cast<uint32_t *>(dst) = colp[j];
-            dst += a.ld_codes_t;
-        }
-    }
-    if (rg == 0 && (cc & 3) == 0) {
+    if (col_ok && rg == 0 && (cc & 3) == 0) {
         const uint8_t sbyte = finite ? (uint8_t)(e + 127) : (uint8_t)0xFF;
         const int64_t rb = strip_r >> 5, cb = c0 >> 5;
         if (a.scales && rb < a.nbr) a.scales[rb * a.ld_scales + cb] = sbyte;
@@ -264,36 +381,40 @@ __global__ __launch_bounds__(256) void fp4_quantize_kernel(QuantArgs a)
 }
 
 template <typename T, bool VEC, bool SR, bool A8, bool G>
-hipError_t launch_t(const QuantArgs &a, int64_t nblocks, hipStream_t s)
+hipError_t launch_t(const QuantArgs &a, hipStream_t s)
 {
-    hipLaunchKernelGGL((fp4_quantize_kernel<T, VEC, SR, A8, G>), dim3((unsigned)nblocks), dim3(256), 0, s, a);
+    // round to nearest is bound by memory traffic: 256-column tiles write whole
+    // 128-byte lines of codes.  Stochastic rounding is bound by its Philox work
+    // and keeps 4-wave workgroups for occupancy.
+    constexpr int WC = SR ? 1 : 2;
+    const int64_t nb = (a.rows_pad / kTile) * ((a.cols_pad + 128 * WC - 1) / (128 * WC));
+    hipLaunchKernelGGL((fp4_quantize_kernel<T, VEC, SR, A8, G, WC>), dim3((unsigned)nb), dim3(256 * WC), 0, s, a);
     return hipGetLastError();
 }
 
 template <typename T, bool G>
-hipError_t launch_dtype(const QuantArgs &a, bool vec, bool sr, bool a8, int64_t nb, hipStream_t s)
+hipError_t launch_dtype(const QuantArgs &a, bool vec, bool sr, bool a8, hipStream_t s)
 {
     if (vec) {
-        if (!sr) return launch_t<T, true, false, true, G>(a, nb, s);
-        return a8 ? launch_t<T, true, true, true, G>(a, nb, s) : launch_t<T, true, true, false, G>(a, nb, s);
+        if (!sr) return launch_t<T, true, false, true, G>(a, s);
+        return a8 ? launch_t<T, true, true, true, G>(a, s) : launch_t<T, true, true, false, G>(a, s);
     }
-    return sr ? launch_t<T, false, true, true, G>(a, nb, s) : launch_t<T, false, false, true, G>(a, nb, s);
+    return sr ? launch_t<T, false, true, true, G>(a, s) : launch_t<T, false, false, true, G>(a, s);
 }
 
 }  // namespace
 
 hipError_t launch_fp4_quantize(const QuantArgs &a, int dtype_bytes, bool sr, hipStream_t stream)
 {
-    const int64_t nb = (a.rows_pad / kTile) * (a.cols_pad / kTile);
     const uintptr_t base = reinterpret_cast<uintptr_t>(a.x);
     const bool vec = a.stride_c == 1 && (base % 16) == 0 && ((a.stride_r * dtype_bytes) % 16) == 0;
     const bool a8 = (a.stride_r % 8) == 0 && (a.index_base % 8) == 0;
     const bool grouped = a.seg_offsets != nullptr;
     if (dtype_bytes == 4)
-        return grouped ? launch_dtype<float, true>(a, vec, sr, a8, nb, stream)
-                       : launch_dtype<float, false>(a, vec, sr, a8, nb, stream);
-    return grouped ? launch_dtype<uint16_t, true>(a, vec, sr, a8, nb, stream)
-                   : launch_dtype<uint16_t, false>(a, vec, sr, a8, nb, stream);
+        return grouped ? launch_dtype<float, true>(a, vec, sr, a8, stream)
+                       : launch_dtype<float, false>(a, vec, sr, a8, stream);
+    return grouped ? launch_dtype<uint16_t, true>(a, vec, sr, a8, stream)
+                   : launch_dtype<uint16_t, false>(a, vec, sr, a8, stream);
 }
 
 }  // namespace q2d
