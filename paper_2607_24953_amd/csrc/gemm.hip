@@ -569,6 +569,157 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(GemmArgs g, i
     }
 }
 
+// Large-tile MXFP8 kernel (the query/key projections): 256 x 256 output tile,
+// 4 waves of 128 x 128, E4M3 operands (8 VGPRs per lane per MFMA, 64 cycles
+// each).  A stage holds one K-tile of 64 values: 64 bytes per row of A and of B
+// (16 KB each) and the rows' scale words (the 4-byte word holding this
+// K-tile's two 1x32 scales; 1 KB each), filled by global_load_lds DMA through
+// a ring of kStages stages.  Each iteration runs the 16 MFMAs of one K-tile
+// while the next K-tile's fragments are read and the stage just consumed is
+// refilled; the fragment buffers alternate between two register sets.
+constexpr int kDma8 = 10;                 // per wave per K-tile: 4 A, 4 B, 1 A-scale, 1 B-scale
+constexpr int kStage8 = 2 * kCodeBytes + 2048;
+
+template <bool BF16OUT, bool ACC>
+__global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, int tiles_m, int tiles_n)
+{
+    using F = Fmt<kFmtMxfp8>;
+    constexpr int RB = 64;                          // bytes per row per K-tile of 64
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStage8];
+
+    int tm, tn;
+    {
+        int64_t tm64, tn64;
+        tile_coords(tiles_m, tiles_n, tm64, tn64);
+        tm = (int)tm64; tn = (int)tn64;
+    }
+    const int64_t m0 = (int64_t)tm * BM2, n0 = (int64_t)tn * BN2;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+    const int half = lane >> 5;
+    const uint32_t nk = (uint32_t)(g.K / 64);       // K is a multiple of 128
+
+    // codes: DMA j of this wave fills bytes [(4j + wave) * 1024, +1024) of an
+    // operand stage (rows 16 (4j + wave) + lane / 4, physical chunk lane % 4,
+    // the 64-byte-row swizzle of the E2M1 kernel); scales: the wave's DMA
+    // fills rows 64 wave + lane of the stage's A and B scale words
+    uint32_t offA[4], offB[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int row = 16 * (4 * j + wave) + (lane >> 2);
+        const int c = (lane & 3) ^ Fmt<kFmtFp4Block2D>::swz(row);
+        int64_t ra = m0 + row; ra = ra < g.M ? ra : g.M - 1;
+        int64_t rb = n0 + row; rb = rb < g.N ? rb : g.N - 1;
+        offA[j] = (uint32_t)(ra * g.lda + c * 16);
+        offB[j] = (uint32_t)(rb * g.ldb + c * 16);
+    }
+    const uint8_t *srcSA, *srcSB;
+    {
+        int64_t ra = m0 + 64 * wave + lane; ra = ra < g.M ? ra : g.M - 1;
+        int64_t rb = n0 + 64 * wave + lane; rb = rb < g.N ? rb : g.N - 1;
+        srcSA = g.sa + ra * g.ldsa;
+        srcSB = g.sb + rb * g.ldsb;
+    }
+    const uint32_t lds0 = (uint32_t)(uintptr_t)&smem[0];
+    const int sw = Fmt<kFmtFp4Block2D>::swz(lane & 31);
+    const int rd_a = (wm * 128 + (lane & 31)) * RB;
+    const int rd_b = kCodeBytes + (wn * 128 + (lane & 31)) * RB;
+    const int rs_a = 2 * kCodeBytes + (wm * 128 + (lane & 31)) * 4;
+    const int rs_b = 2 * kCodeBytes + 1024 + (wn * 128 + (lane & 31)) * 4;
+
+    v16f acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    auto dma = [&](uint32_t t, int part) {          // part 0..9
+        const uint32_t tt = t < nk ? t : nk - 1;
+        const uint32_t stage = lds0 + (t % kStages) * kStage8;
+        if (part < 8) {
+            const int jj = part >> 1;
+            if ((part & 1) == 0) lds_dma16(g.a + tt * RB, offA[jj], stage + (4 * jj + wave) * 1024);
+            else lds_dma16(g.b + tt * RB, offB[jj], stage + kCodeBytes + (4 * jj + wave) * 1024);
+        } else if (part == 8) {
+            lds_dma4(srcSA + (tt >> 1) * 4, stage + 2 * kCodeBytes + wave * 256);
+        } else {
+            lds_dma4(srcSB + (tt >> 1) * 4, stage + 2 * kCodeBytes + 1024 + wave * 256);
+        }
+    };
+    // fragments of one K-tile: A tile i / B tile j as two 16-byte chunks
+    // (chunks half and 2 + half of the row) and the rows' scale words; each
+    // is re-read from the next K-tile's stage right after its last use
+    v8i fa[4], fb[4];
+    uint32_t sa[4], sb[4];
+    const int c0 = (half ^ sw) * 16, c1 = ((2 + half) ^ sw) * 16;
+#define Q2D_RD8(dst, base, row_off)                                                                  \
+    do {                                                                                             \
+        const uint4 x0_ = *reinterpret_cast<const uint4 *>((base) + (row_off) + c0);                 \
+        const uint4 x1_ = *reinterpret_cast<const uint4 *>((base) + (row_off) + c1);                 \
+        dst[0] = (int)x0_.x; dst[1] = (int)x0_.y; dst[2] = (int)x0_.z; dst[3] = (int)x0_.w;          \
+        dst[4] = (int)x1_.x; dst[5] = (int)x1_.y; dst[6] = (int)x1_.z; dst[7] = (int)x1_.w;          \
+    } while (0)
+
+    if (nk > 0) {
+        for (int t = 0; t < kStages; ++t)
+            for (int p = 0; p < kDma8; ++p) dma((uint32_t)t, p);
+        wait_vmcnt<(kStages - 1) * kDma8>();
+        block_barrier();
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            Q2D_RD8(fa[i], smem, rd_a + i * 32 * RB);
+            Q2D_RD8(fb[i], smem, rd_b + i * 32 * RB);
+            sa[i] = *reinterpret_cast<const uint32_t *>(smem + rs_a + i * 32 * 4);
+            sb[i] = *reinterpret_cast<const uint32_t *>(smem + rs_b + i * 32 * 4);
+        }
+        for (uint32_t kt = 0; kt < nk; ++kt) {
+            __builtin_amdgcn_s_waitcnt(0xC07F);                 // lgkmcnt(0): this K-tile's reads done
+            wait_vmcnt<(kStages - 2) * kDma8>();                // K-tile kt + 1 landed
+            block_barrier();
+            const uint8_t *sn = smem + ((kt + 1) % kStages) * kStage8;   // past the last K-tile: unused reads
+            const int byte = 2 * (kt & 1) + half;               // this K-tile's scale in the row word
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int sa_ = (int)((sa[i] >> (8 * byte)) & 0xFFu);
+                    const int sb_ = (int)((sb[j] >> (8 * byte)) & 0xFFu);
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[j], acc[i][j],
+                                                                                F::kCbsz, F::kCbsz, 0, sa_, 0, sb_);
+                    __builtin_amdgcn_sched_barrier(0);
+                    const int q = 4 * i + j;
+                    if (q < 10) {
+                        dma(kt + kStages, q);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                    if (i == 3) {                               // last use of B tile j
+                        Q2D_RD8(fb[j], sn, rd_b + j * 32 * RB);
+                        sb[j] = *reinterpret_cast<const uint32_t *>(sn + rs_b + j * 32 * 4);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+                // last use of A tile i
+                Q2D_RD8(fa[i], sn, rd_a + i * 32 * RB);
+                sa[i] = *reinterpret_cast<const uint32_t *>(sn + rs_a + i * 32 * 4);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        wait_vmcnt<0>();
+    }
+#undef Q2D_RD8
+
+    const int64_t row0 = m0 + wm * 128 + 4 * half;
+    const int64_t col0 = n0 + wn * 128 + (lane & 31);
+    if (m0 + BM2 <= g.M && n0 + BN2 <= g.N) {
+        store_tile<BF16OUT, ACC, false>(acc, g, row0, col0);
+    } else {
+        store_tile<BF16OUT, ACC, true>(acc, g, row0, col0);
+    }
+}
+
 template <bool BF, int GMODE>
 hipError_t launch_256(const GemmArgs &g, const GroupedArgs &gr, int tm, int tn, int grid, hipStream_t s)
 {
@@ -602,6 +753,17 @@ hipError_t launch_gemm(const GemmArgs &g, int fmt, int c_is_bf16, hipStream_t st
     }
     if (fmt == kFmtFp4Block2D)
         return c_is_bf16 ? launch_t<kFmtFp4Block2D, true>(g, stream) : launch_t<kFmtFp4Block2D, false>(g, stream);
+    if (off32 && ((g.M + BM2 - 1) / BM2) * ((g.N + BN2 - 1) / BN2) >= 128) {
+        const int tm = (int)((g.M + BM2 - 1) / BM2), tn = (int)((g.N + BN2 - 1) / BN2);
+        if (c_is_bf16) {
+            if (g.accumulate) hipLaunchKernelGGL((gemm_fp8_256_kernel<true, true>), dim3(tm * tn), dim3(kThreads), 0, stream, g, tm, tn);
+            else hipLaunchKernelGGL((gemm_fp8_256_kernel<true, false>), dim3(tm * tn), dim3(kThreads), 0, stream, g, tm, tn);
+        } else {
+            if (g.accumulate) hipLaunchKernelGGL((gemm_fp8_256_kernel<false, true>), dim3(tm * tn), dim3(kThreads), 0, stream, g, tm, tn);
+            else hipLaunchKernelGGL((gemm_fp8_256_kernel<false, false>), dim3(tm * tn), dim3(kThreads), 0, stream, g, tm, tn);
+        }
+        return hipGetLastError();
+    }
     return c_is_bf16 ? launch_t<kFmtMxfp8, true>(g, stream) : launch_t<kFmtMxfp8, false>(g, stream);
 }
 

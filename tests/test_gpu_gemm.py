@@ -122,8 +122,11 @@ def test_linear_fwd_bwd(q2d, T, N, K):
     assert rel_frob(dW.cpu().numpy(), ref["dW"]) <= TOL
 
 
-@pytest.mark.parametrize("M,N,K", [(128, 256, 256), (300, 200, 160), (1000, 300, 2000)])
-@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 1)])
+@pytest.mark.parametrize("M,N,K", [(128, 256, 256), (300, 200, 160), (1000, 300, 2000),
+                                   # enough 256 x 256 tiles for the large-tile kernel: ragged
+                                   # edges, K shorter than its 4-stage ring (256 = 4 K-tiles of 64)
+                                   (4096, 2048, 1024), (4000, 2100, 640), (2048, 4224, 256)])
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 1), (1, 0)])
 def test_gemm_mxfp8(q2d, M, N, K, ta, tb):
     a_shape = (K, M) if ta else (M, K)
     b_shape = (K, N) if tb else (N, K)
@@ -198,4 +201,39 @@ def test_full_7b_launch_configuration(q2d):
         got_dw = dW[torch.from_numpy(rows_w).to(DEV)].cpu().numpy()
         assert rel_frob(got_dw, ref_dw) <= TOL
         del Y, dX, dW, qX, qW, qdY, Wf, Wt, Xt
+    torch.cuda.empty_cache()
+
+
+def test_full_mixed_7b_qk_launch_configuration(q2d):
+    """The MXFP8 query/key GEMMs of the mixed 7B block at full size (tokens 16384,
+    hidden 4096; bf16 Y and dX, fp32 dW), 32 sampled rows each, against float64
+    products of the oracle's MXFP8 operands within the FP8 MFMA bound."""
+    w = synth.mixed_7b(device=DEV)
+    rng = np.random.default_rng(2)
+    X = w.tensors["X_qkv"]
+    qX = q2d.mxfp8_quantize(X)
+    oX = oracle.quantize_mxfp8(X.cpu())
+    assert_same_bytes(gpu_buffers(qX), oX, "X_qkv mxfp8")
+    Xt = oracle.operand(oX, True, "mxfp8")
+    for name in ("q", "k"):
+        W, dY = w.tensors["W_" + name], w.tensors["dY_" + name]
+        qW, qdY = q2d.mxfp8_quantize(W), q2d.mxfp8_quantize(dY)
+        oW, odY = oracle.quantize_mxfp8(W.cpu()), oracle.quantize_mxfp8(dY.cpu())
+        assert_same_bytes(gpu_buffers(qW), oW, "W mxfp8")
+        assert_same_bytes(gpu_buffers(qdY), odY, "dY mxfp8")
+        print("mixed 7B %s projection: GEMMs" % name, flush=True)
+        Y = q2d.q2d_gemm(qX, 0, qW, 0, out_dtype=torch.float32)
+        dX = q2d.q2d_gemm(qdY, 0, qW, 1, out_dtype=torch.float32)
+        dW = q2d.q2d_gemm(qdY, 1, qX, 1, out_dtype=torch.float32)
+        Wf, Wt = oracle.operand(oW, False, "mxfp8"), oracle.operand(oW, True, "mxfp8")
+        A = oracle.operand(oX, False, "mxfp8")
+        dYf, dYt = oracle.operand(odY, False, "mxfp8"), oracle.operand(odY, True, "mxfp8")
+        for got, a, b in ((Y, A, Wf), (dX, dYf, Wt), (dW, dYt, Xt)):
+            rows = np.sort(rng.choice(a.shape[0], 32, replace=False))
+            ref = a[rows] @ b.T
+            bound = 2.0 ** -11 * (np.abs(a[rows]) @ np.abs(b).T) + 1e-30
+            g = got[torch.from_numpy(rows).to(DEV)].cpu().numpy().astype(np.float64)
+            assert np.all(np.abs(g - ref) <= bound), float((np.abs(g - ref) / bound).max())
+            assert rel_frob(g, ref) <= 5e-4
+        del qW, qdY, Y, dX, dW
     torch.cuda.empty_cache()
