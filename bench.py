@@ -123,12 +123,15 @@ def kind_of(kernel_name: str):
     m = re.search(r"gemm_fp4_256_kernel<([^>]*)>", kernel_name)
     if m:
         return "gemm_fp4" if m.group(1).split(",")[2].strip() == "0" else "gemm_fp4_grouped"
+    if "gemm_fp8_256_kernel" in kernel_name:
+        return "gemm_fp8"
     m = re.search(r"gemm_kernel<(\d)", kernel_name)
     if m:
         return "gemm_fp4" if m.group(1) == "0" else "gemm_fp8"
     m = re.search(r"fp4_quantize_kernel<([^>]*)>", kernel_name)
     if m:
-        return "quant_fp4_grouped" if m.group(1).split(",")[-1].strip() == "true" else "quant_fp4"
+        # template arguments: element type, VEC, SR, ALIGNED8, GROUPED, column waves
+        return "quant_fp4_grouped" if m.group(1).split(",")[4].strip() == "true" else "quant_fp4"
     if "mxfp8_quantize_kernel" in kernel_name:
         return "quant_mxfp8"
     return None
