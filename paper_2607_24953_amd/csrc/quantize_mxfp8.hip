@@ -7,8 +7,13 @@
 // which is what the data-gradient and weight-gradient GEMMs read.
 //
 // Same work split as the FP4 quantizer: 4 waves x (32 x 128) strips, each lane
-// an 8 x 8 sub-block.  A 1 x 32 row block spans the 4 lanes that differ in lane
-// bits 0-1; a 32 x 1 column block spans the 4 lanes that differ in bits 4-5.
+// an 8 x 8 sub-block (bf16 rows kept packed two elements per register).  A
+// 1 x 32 row block spans the 4 lanes that differ in lane bits 0-1; a 32 x 1
+// column block spans the 4 lanes that differ in bits 4-5.  The E4M3 codes come
+// from gfx950's v_cvt_scalef32_pk_fp8_{bf16,f32} (round to nearest even of
+// x / S, two elements per instruction).  Rowwise codes leave as 8-byte stores
+// (16 lanes cover a 128-byte row); the colwise codes and both scale grids go
+// through LDS and leave as 16- and 4-byte stores.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -18,15 +23,36 @@ namespace {
 
 constexpr int kTile = 128;
 
+typedef short s2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ uint32_t load_bits(const void *x, bool is_f32, int64_t idx)
 {
     if (is_f32) return f_bits(reinterpret_cast<const float *>(x)[idx]);
     return (uint32_t)reinterpret_cast<const uint16_t *>(x)[idx] << 16;
 }
 
+// E4M3 pair (low element first) into 16-bit word SEL of `old`
+template <bool SEL>
+__device__ __forceinline__ uint32_t fp8_pair_bf16(uint32_t old, uint32_t packed, float scale)
+{
+    const s2v r = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(__builtin_bit_cast(s2v, old),
+                                                            __builtin_bit_cast(bf16x2, packed), scale, SEL);
+    return __builtin_bit_cast(uint32_t, r);
+}
+template <bool SEL>
+__device__ __forceinline__ uint32_t fp8_pair_f32(uint32_t old, uint32_t lo, uint32_t hi, float scale)
+{
+    const s2v r = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(__builtin_bit_cast(s2v, old), bits_f(lo), bits_f(hi),
+                                                           scale, SEL);
+    return __builtin_bit_cast(uint32_t, r);
+}
+
 template <bool F32, bool VEC>
 __global__ __launch_bounds__(256) void mxfp8_quantize_kernel(const QuantArgs a)
 {
+    constexpr bool PK = !F32;                 // bf16: two elements per register
+    constexpr int NV = PK ? 4 : 8;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int64_t tiles_c = a.cols_pad / kTile;
@@ -36,100 +62,149 @@ __global__ __launch_bounds__(256) void mxfp8_quantize_kernel(const QuantArgs a)
     const int rg = lane >> 4, cc = lane & 15;
     const int64_t r0 = strip_r + 8 * rg;
     const int64_t c0 = tc * kTile + 8 * cc;
-    const bool vec = VEC && c0 + 8 <= a.cols;
 
-    uint32_t v[8][8];
+    // ---- load the 8 x 8 sub-block (0 outside R x C)
+    uint32_t v[8][NV];
+    if (VEC && c0 + 8 <= a.cols) {
+        const uint8_t *xr = reinterpret_cast<const uint8_t *>(a.x) + (r0 * a.stride_r + c0) * (F32 ? 4 : 2);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int64_t r = r0 + i;
-        if (vec && r < a.rows) {
-            if (F32) {
-                const float *p = reinterpret_cast<const float *>(a.x) + r * a.stride_r + c0;
-                const uint4 u0 = *reinterpret_cast<const uint4 *>(p);
-                const uint4 u1 = *reinterpret_cast<const uint4 *>(p + 4);
-                v[i][0] = u0.x; v[i][1] = u0.y; v[i][2] = u0.z; v[i][3] = u0.w;
-                v[i][4] = u1.x; v[i][5] = u1.y; v[i][6] = u1.z; v[i][7] = u1.w;
-            } else {
-                const uint16_t *p = reinterpret_cast<const uint16_t *>(a.x) + r * a.stride_r + c0;
-                const uint4 u = *reinterpret_cast<const uint4 *>(p);
-                v[i][0] = u.x << 16; v[i][1] = u.x & 0xFFFF0000u;
-                v[i][2] = u.y << 16; v[i][3] = u.y & 0xFFFF0000u;
-                v[i][4] = u.z << 16; v[i][5] = u.z & 0xFFFF0000u;
-                v[i][6] = u.w << 16; v[i][7] = u.w & 0xFFFF0000u;
+        for (int i = 0; i < 8; ++i) {
+            uint4 q0 = make_uint4(0u, 0u, 0u, 0u), q1 = q0;
+            if (r0 + i < a.rows) {
+                q0 = *reinterpret_cast<const uint4 *>(xr);
+                if (F32) q1 = *reinterpret_cast<const uint4 *>(xr + 16);
             }
-        } else {
+            v[i][0] = q0.x; v[i][1] = q0.y; v[i][2] = q0.z; v[i][3] = q0.w;
+            if (F32) { v[i][NV - 4] = q1.x; v[i][NV - 3] = q1.y; v[i][NV - 2] = q1.z; v[i][NV - 1] = q1.w; }
+            xr += a.stride_r * (F32 ? 4 : 2);
+        }
+    } else {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int64_t c = c0 + j;
-                v[i][j] = (r < a.rows && c < a.cols) ? load_bits(a.x, F32, r * a.stride_r + c * a.stride_c) : 0u;
+        for (int i = 0; i < 8; ++i) {
+            const int64_t r = r0 + i;
+#pragma unroll
+            for (int k = 0; k < NV; ++k) {
+                if (PK) {
+                    const int64_t c = c0 + 2 * k;
+                    const uint32_t lo = (r < a.rows && c < a.cols) ? load_bits(a.x, false, r * a.stride_r + c * a.stride_c) : 0u;
+                    const uint32_t hi = (r < a.rows && c + 1 < a.cols) ? load_bits(a.x, false, r * a.stride_r + (c + 1) * a.stride_c) : 0u;
+                    v[i][k] = (lo >> 16) | hi;
+                } else {
+                    const int64_t c = c0 + k;
+                    v[i][k] = (r < a.rows && c < a.cols) ? load_bits(a.x, true, r * a.stride_r + c * a.stride_c) : 0u;
+                }
             }
         }
     }
+    // float32 bit pattern of element (i, j)
+    auto elem = [&](int i, int j) -> uint32_t {
+        if (PK) return (j & 1) ? (v[i][j >> 1] & 0xFFFF0000u) : (v[i][j >> 1] << 16);
+        return v[i][j];
+    };
 
-    // rowwise (1 x 32) maxima: one per sub-block row, shared by lanes ^1, ^2
+    // ---- block maxima on |bits|: rows (1 x 32, lanes ^1 ^2), columns (32 x 1, lanes ^16 ^32)
     uint32_t rmax[8], cmax[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         uint32_t m = 0;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) m = max(m, v[i][j] & 0x7FFFFFFFu);
+        for (int j = 0; j < 8; ++j) m = max(m, elem(i, j) & 0x7FFFFFFFu);
         m = max(m, (uint32_t)__shfl_xor((int)m, 1));
         m = max(m, (uint32_t)__shfl_xor((int)m, 2));
         rmax[i] = m;
     }
-    // colwise (32 x 1) maxima: one per sub-block column, shared by lanes ^16, ^32
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         uint32_t m = 0;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) m = max(m, v[i][j] & 0x7FFFFFFFu);
+        for (int i = 0; i < 8; ++i) m = max(m, elem(i, j) & 0x7FFFFFFFu);
         m = max(m, (uint32_t)__shfl_xor((int)m, 16));
         m = max(m, (uint32_t)__shfl_xor((int)m, 32));
         cmax[j] = m;
     }
 
-    // ---- rowwise copy
-    if (a.codes) {
+    __shared__ uint32_t st_c[kTile][33];      // column c: 128 codes (rows of the tile) + pad
+    __shared__ uint8_t st_sr[kTile][4];       // row scales of the tile's four 1 x 32 blocks
+    __shared__ uint8_t st_sc[kTile][4];       // column scales of the four 32 x 1 blocks
+
+    // ---- rowwise copy: 8 codes of row i (two words), stored directly
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int64_t r = r0 + i;
-            const bool finite = rmax[i] < 0x7F800000u;
-            const int e = fp8_block_exponent(rmax[i]);
-            const float inv = inv_pow2(e);
-            uint32_t lo = 0, hi = 0;
+    for (int i = 0; i < 8; ++i) {
+        const int64_t r = r0 + i;
+        const bool finite = rmax[i] < 0x7F800000u;
+        const int e = fp8_block_exponent(rmax[i]);
+        const float scale = bits_f((uint32_t)(127 + e) << 23);
+        uint32_t lo = 0, hi = 0;
+        if (PK) {
+            lo = fp8_pair_bf16<false>(lo, v[i][0], scale);
+            lo = fp8_pair_bf16<true>(lo, v[i][PK ? 1 : 0], scale);
+            hi = fp8_pair_bf16<false>(hi, v[i][PK ? 2 : 0], scale);
+            hi = fp8_pair_bf16<true>(hi, v[i][PK ? 3 : 0], scale);
+        } else {
+            lo = fp8_pair_f32<false>(lo, elem(i, 0), elem(i, 1), scale);
+            lo = fp8_pair_f32<true>(lo, elem(i, 2), elem(i, 3), scale);
+            hi = fp8_pair_f32<false>(hi, elem(i, 4), elem(i, 5), scale);
+            hi = fp8_pair_f32<true>(hi, elem(i, 6), elem(i, 7), scale);
+        }
+        if (!finite) { lo = 0; hi = 0; }
+        if (a.codes && r < a.rows) *reinterpret_cast<uint2 *>(a.codes + r * a.ld_codes + c0) = make_uint2(lo, hi);
+        if ((cc & 3) == 0) st_sr[wave * 32 + 8 * rg + i][cc >> 2] = finite ? (uint8_t)(e + 127) : (uint8_t)0xFF;
+    }
+    // ---- colwise copy: 8 codes of column j (rows r0 .. r0+7) into LDS
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const uint32_t b = v[i][j];
-                const uint32_t code = finite ? (((b >> 24) & 0x80u) | e4m3_rne(bits_f(b & 0x7FFFFFFFu) * inv)) : 0u;
-                if (j < 4) lo |= code << (8 * j); else hi |= code << (8 * (j - 4));
-            }
-            if (r < a.rows) {
-                *reinterpret_cast<uint2 *>(a.codes + r * a.ld_codes + c0) = make_uint2(lo, hi);
-                if ((cc & 3) == 0)
-                    a.scales[r * a.ld_scales + (c0 >> 5)] = finite ? (uint8_t)(e + 127) : (uint8_t)0xFF;
+    for (int j = 0; j < 8; ++j) {
+        const bool finite = cmax[j] < 0x7F800000u;
+        const int e = fp8_block_exponent(cmax[j]);
+        const float scale = bits_f((uint32_t)(127 + e) << 23);
+        uint32_t lo = 0, hi = 0;
+        if (PK) {
+            const int k = j >> 1;
+            auto pr = [&](int m) -> uint32_t {
+                const uint32_t x0 = v[2 * m][k], x1 = v[2 * m + 1][k];
+                return (j & 1) ? ((x0 >> 16) | (x1 & 0xFFFF0000u)) : ((x0 & 0xFFFFu) | (x1 << 16));
+            };
+            lo = fp8_pair_bf16<false>(lo, pr(0), scale);
+            lo = fp8_pair_bf16<true>(lo, pr(1), scale);
+            hi = fp8_pair_bf16<false>(hi, pr(2), scale);
+            hi = fp8_pair_bf16<true>(hi, pr(3), scale);
+        } else {
+            lo = fp8_pair_f32<false>(lo, elem(0, j), elem(1, j), scale);
+            lo = fp8_pair_f32<true>(lo, elem(2, j), elem(3, j), scale);
+            hi = fp8_pair_f32<false>(hi, elem(4, j), elem(5, j), scale);
+            hi = fp8_pair_f32<true>(hi, elem(6, j), elem(7, j), scale);
+        }
+        if (!finite) { lo = 0; hi = 0; }
+        st_c[8 * cc + j][wave * 8 + 2 * rg] = lo;
+        st_c[8 * cc + j][wave * 8 + 2 * rg + 1] = hi;
+        if (rg == 0) st_sc[8 * cc + j][wave] = finite ? (uint8_t)(e + 127) : (uint8_t)0xFF;
+    }
+    __syncthreads();
+    // ---- colwise codes (columns c < C, 16 bytes per lane) and both scale grids
+    if (a.codes_t) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int item = threadIdx.x + 256 * q;
+            const int line = item >> 3, part = item & 7;
+            const int64_t c = tc * kTile + line;
+            if (c < a.cols) {
+                const uint4 w = make_uint4(st_c[line][4 * part], st_c[line][4 * part + 1],
+                                           st_c[line][4 * part + 2], st_c[line][4 * part + 3]);
+                *reinterpret_cast<uint4 *>(a.codes_t + c * a.ld_codes_t + tr * kTile + part * 16) = w;
             }
         }
     }
-    // ---- colwise copy, stored transposed
-    if (a.codes_t) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int64_t c = c0 + j;
-            const bool finite = cmax[j] < 0x7F800000u;
-            const int e = fp8_block_exponent(cmax[j]);
-            const float inv = inv_pow2(e);
-            uint32_t lo = 0, hi = 0;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const uint32_t b = v[i][j];
-                const uint32_t code = finite ? (((b >> 24) & 0x80u) | e4m3_rne(bits_f(b & 0x7FFFFFFFu) * inv)) : 0u;
-                if (i < 4) lo |= code << (8 * i); else hi |= code << (8 * (i - 4));
-            }
-            if (c < a.cols) {
-                *reinterpret_cast<uint2 *>(a.codes_t + c * a.ld_codes_t + r0) = make_uint2(lo, hi);
-                if (rg == 0)
-                    a.scales_t[c * a.ld_scales_t + (strip_r >> 5)] = finite ? (uint8_t)(e + 127) : (uint8_t)0xFF;
-            }
+    {
+        const int t = threadIdx.x & 127;
+        if (threadIdx.x < 128) {
+            const int64_t r = tr * kTile + t;
+            if (a.scales && r < a.rows)
+                *reinterpret_cast<uint32_t *>(a.scales + r * a.ld_scales + tc * 4) =
+                    *reinterpret_cast<const uint32_t *>(&st_sr[t][0]);
+        } else {
+            const int64_t c = tc * kTile + t;
+            if (a.scales_t && c < a.cols)
+                *reinterpret_cast<uint32_t *>(a.scales_t + c * a.ld_scales_t + tr * 4) =
+                    *reinterpret_cast<const uint32_t *>(&st_sc[t][0]);
         }
     }
 }
