@@ -57,8 +57,8 @@ KIND_PEAK = {"gemm_fp4": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
              "quant_fp4": ("hbm", PEAK_HBM_GBS, "GB/s"),
              "quant_fp4_grouped": ("hbm", PEAK_HBM_GBS, "GB/s"),
              "quant_mxfp8": ("hbm", PEAK_HBM_GBS, "GB/s")}
-KIND_KERNEL = {"gemm_fp4": "gemm_fp4_256_kernel", "gemm_fp4_grouped": "gemm_fp4_256_kernel (grouped)",
-               "gemm_fp8": "gemm_kernel<MXFP8>", "quant_fp4": "fp4_quantize_kernel",
+KIND_KERNEL = {"gemm_fp4": "gemm_fp4_persistent_kernel", "gemm_fp4_grouped": "gemm_fp4_persistent_kernel (grouped)",
+               "gemm_fp8": "gemm_fp8_256_kernel", "quant_fp4": "fp4_quantize_kernel",
                "quant_fp4_grouped": "fp4_quantize_kernel (grouped)",
                "quant_mxfp8": "mxfp8_quantize_kernel"}
 
@@ -120,7 +120,7 @@ def kind_hash(kind: str) -> str:
 def kind_of(kernel_name: str):
     """Launch kind of a libq2d kernel from its (demangled) name, None for other kernels."""
     import re
-    m = re.search(r"gemm_fp4_256_kernel<([^>]*)>", kernel_name)
+    m = re.search(r"gemm_fp4_persistent_kernel<([^>]*)>", kernel_name)
     if m:
         return "gemm_fp4" if m.group(1).split(",")[2].strip() == "0" else "gemm_fp4_grouped"
     if "gemm_fp8_256_kernel" in kernel_name:
@@ -342,7 +342,7 @@ def cpu_baseline(w, tokens: int):
 
 PROFILE_WORKLOADS = ("dense_7b", "moe_30b", "mixed_7b")
 PROFILE_FILES = {
-    "dense_7b": [("gemm_fp4_256_kernel.dense_7b.md", ("gemm_fp4",)),
+    "dense_7b": [("gemm_fp4_persistent_kernel.dense_7b.md", ("gemm_fp4",)),
                  ("fp4_quantize_kernel.dense_7b.md", ("quant_fp4",))],
     "moe_30b": [("grouped_fp4_kernels.moe_30b.md", ("gemm_fp4_grouped", "quant_fp4_grouped", "quant_fp4"))],
     "mixed_7b": [("mxfp8_kernels.mixed_7b.md", ("gemm_fp8", "quant_mxfp8", "gemm_fp4", "quant_fp4"))],

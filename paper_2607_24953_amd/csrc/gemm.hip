@@ -17,6 +17,7 @@
 // operand reads (32 consecutive rows, same chunk) hit distinct banks.
 // Workgroups are remapped so that each XCD (one L2) walks a contiguous band of
 // output tiles, grouped by 8 row tiles for operand reuse.
+#include <atomic>
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -59,12 +60,11 @@ struct Fmt<kFmtMxfp8> {
     static __device__ __forceinline__ int chunk(int ks, int half, int h) { return 4 * ks + 2 * h + half; }
 };
 
-__device__ __forceinline__ void tile_coords(int64_t tiles_m, int64_t tiles_n, int64_t &tm, int64_t &tn)
+__device__ __forceinline__ void tile_coords_of(int64_t bid, int64_t tiles_m, int64_t tiles_n, int64_t &tm, int64_t &tn)
 {
     // Hardware dispatch sends consecutive workgroups to consecutive XCDs; give
     // every XCD a contiguous range of the tile order instead.
     const int64_t nb = tiles_m * tiles_n;
-    const int64_t bid = blockIdx.x;
     const int64_t xcd = bid % kXcds, local = bid / kXcds;
     const int64_t per = nb / kXcds, rem = nb % kXcds;
     const int64_t t = xcd * per + (xcd < rem ? xcd : rem) + local;
@@ -76,6 +76,11 @@ __device__ __forceinline__ void tile_coords(int64_t tiles_m, int64_t tiles_n, in
     const int64_t in = t - grp * span;
     tm = first + in % gsz;
     tn = in / gsz;
+}
+
+__device__ __forceinline__ void tile_coords(int64_t tiles_m, int64_t tiles_n, int64_t &tm, int64_t &tn)
+{
+    tile_coords_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
 }
 
 template <int FMT, bool BF16OUT>
@@ -273,17 +278,6 @@ __device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)
 
 __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-__device__ __forceinline__ void grouped_coords32(int t, int tiles_m, int tiles_n, int &tm, int &tn)
-{
-    const int span = kGroupM * tiles_n;
-    const int grp = t / span;
-    const int first = grp * kGroupM;
-    const int gsz = (tiles_m - first) < kGroupM ? (tiles_m - first) : kGroupM;
-    const int in = t - grp * span;
-    tm = first + in % gsz;
-    tn = in / gsz;
-}
-
 // Write a wave's 128 x 128 accumulator block (4 x 4 MFMA tiles) to C; CHECK
 // masks rows >= M and columns >= N.  bf16 output rounds to nearest even.
 template <bool BF16OUT, bool ACC, bool CHECK>
@@ -319,24 +313,158 @@ __device__ __forceinline__ void store_tile(v16f (&acc)[4][4], const GemmArgs &g,
         }
 }
 
-// GMODE 0: dense.  GMODE 1: grouped, ragged M.  GMODE 2: grouped, ragged K.
+// Persistent FP4 kernel (the large-tile design above).  The grid holds one
+// workgroup per CU, a multiple of the 8 XCDs so that a workgroup keeps its
+// XCD's share of the tile order; each walks the tiles u = blockIdx.x,
+// blockIdx.x + gridDim.x, ...  The K-tiles of all its tiles form one stream
+// through the LDS ring: the loads of the next tile's first K-tiles are in
+// flight while the current tile finishes and its accumulators are written, so
+// no tile pays the pipeline fill.  Iteration s of the K loop: (A) the 16 MFMAs
+// of K-substep 0 of step s while the fragments of substep 1 are read; wait for
+// step s + 1 and barrier (every wave now holds step s in registers, so its
+// stage is free); (B) the 16 MFMAs of substep 1 while the nine loads of step
+// s + kStages go into that stage and the substep-0 fragments and scale words
+// of step s + 1 are read.  A load cursor runs kStages steps ahead of the
+// MFMAs and addresses each load from the tile it belongs to.  DMA issues and
+// LDS reads sit between MFMAs (sched_barrier pins the order).
+struct TileRef {
+    const uint8_t *a, *sa, *b, *sb;
+    uint8_t *c;
+    int32_t M, N;          // valid rows of op(A) and op(B) (= rows and columns of C)
+    int32_t m0, n0;        // tile origin in C
+    uint32_t nk;           // K-tiles
+};
+
+template <int GMODE, bool BF16OUT>
+struct TileSpace {
+    const GemmArgs &g;
+    const GroupedArgs &gr;
+    int32_t tiles_m, tiles_n;
+    const int32_t *pad_start, *tile_start;
+    uint32_t total;        // tiles (ragged M: row tiles of all experts x column tiles)
+    uint32_t per, rem, span;   // dense: XCD share of the tile order, group span
+
+    __device__ __forceinline__ uint32_t nk_of(uint32_t u) const
+    {
+        if (GMODE != 2) return (uint32_t)(g.K / BK);
+        const uint32_t e = u / (uint32_t)(tiles_m * tiles_n);
+        return (uint32_t)__builtin_amdgcn_readfirstlane((pad_start[e + 1] - pad_start[e]) / BK);
+    }
+    // first tile at or after u (stepping by the grid) with at least one K-tile
+    __device__ __forceinline__ uint32_t valid_from(uint32_t u) const
+    {
+        if (GMODE == 2)
+            while (u < total && nk_of(u) == 0) u += gridDim.x;
+        return u;
+    }
+    __device__ __forceinline__ TileRef ref(uint32_t u) const
+    {
+        TileRef t;
+        const int esize = BF16OUT ? 2 : 4;
+        t.a = g.a; t.sa = g.sa; t.b = g.b; t.sb = g.sb;
+        t.c = reinterpret_cast<uint8_t *>(g.c);
+        t.M = (int32_t)g.M; t.N = (int32_t)g.N; t.nk = (uint32_t)(g.K / BK);
+        int32_t tm, tn;
+        if (GMODE == 0) {
+            // as tile_coords, in 32 bits
+            const uint32_t xcd = u % kXcds, local = u / kXcds;
+            const uint32_t tt = xcd * per + (xcd < rem ? xcd : rem) + local;
+            const uint32_t grp = tt / span, first = grp * kGroupM;
+            const uint32_t gsz = (uint32_t)tiles_m - first < (uint32_t)kGroupM ? (uint32_t)tiles_m - first : kGroupM;
+            const uint32_t in = tt - grp * span;
+            tm = (int32_t)(first + in % gsz);
+            tn = (int32_t)(in / gsz);
+        } else if (GMODE == 1) {
+            const int32_t rt = (int32_t)(u / (uint32_t)tiles_n);
+            tn = (int32_t)u - rt * tiles_n;
+            const int e = __builtin_amdgcn_readfirstlane(seg_search(tile_start, gr.nseg, rt));
+            tm = rt - __builtin_amdgcn_readfirstlane(tile_start[e]);
+            const int64_t p_e = __builtin_amdgcn_readfirstlane(pad_start[e]);
+            t.a += p_e * g.lda;
+            t.sa += (p_e / 32) * g.ldsa;
+            const int64_t o0 = gr.seg_offsets[e], o1 = gr.seg_offsets[e + 1];
+            t.M = (int32_t)(o1 - o0);
+            t.c += o0 * g.ldc * esize;
+            if (gr.b_group_rows) {
+                t.b += (int64_t)e * gr.b_group_rows * g.ldb;
+                t.sb += ((int64_t)e * gr.b_group_rows / 32) * g.ldsb;
+            } else {
+                t.b += (int64_t)e * gr.b_group_k / 2;
+                t.sb += (int64_t)e * gr.b_group_k / 32;
+            }
+        } else {
+            const uint32_t per_e = (uint32_t)(tiles_m * tiles_n);
+            const int32_t e = (int32_t)(u / per_e);
+            const int32_t rest = (int32_t)(u - (uint32_t)e * per_e);
+            tm = rest / tiles_n;
+            tn = rest - tm * tiles_n;
+            const int64_t p_e = __builtin_amdgcn_readfirstlane(pad_start[e]);
+            t.a += p_e / 2; t.sa += p_e / 32;
+            t.b += p_e / 2; t.sb += p_e / 32;
+            t.nk = (uint32_t)((__builtin_amdgcn_readfirstlane(pad_start[e + 1]) - p_e) / BK);
+            t.c += (int64_t)e * g.M * g.ldc * esize;
+        }
+        t.m0 = tm * BM2;
+        t.n0 = tn * BN2;
+        return t;
+    }
+};
+
+// Write a wave's 128 x 128 accumulator block at cbase (wave-uniform: the
+// block's first element) with 32-bit offsets; CHECK masks rows >= rows_left and
+// columns >= cols_left.  bf16 output rounds to nearest even.
+//
+// Inside the persistent tile loop the row offsets would otherwise be hoisted
+// out of the loop (they depend only on ldc) and all 256 accumulators copied to
+// VGPRs at once; the opaque row stride and the per-element AGPR reads keep the
+// epilogue streaming through a few registers.
+template <bool BF16OUT, bool ACC, bool CHECK>
+__device__ __forceinline__ void store_block(v16f (&acc)[4][4], uint8_t *cbase, uint32_t ldc_bytes, int rows_left,
+                                            int cols_left)
+{
+    const int lane = threadIdx.x & 63;
+    const int col = lane & 31, r4 = 4 * (lane >> 5);
+    const int esize = BF16OUT ? 2 : 4;
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+s"(ldc_bytes));   // and the last MFMA results settle
+    uint32_t rb = (uint32_t)r4 * ldc_bytes + (uint32_t)(col * esize);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int roff = i * 32 + 8 * (r >> 2) + r4 + (r & 3);
+            if (r > 0 || i > 0) rb += (uint32_t)((r & 3) ? 1 : 5) * ldc_bytes;   // next row of this lane
+            if (CHECK && roff >= rows_left) continue;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (CHECK && j * 32 + col >= cols_left) continue;
+                float v;
+                asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(acc[i][j][r]));
+                uint8_t *p = cbase + rb + j * 32 * esize;
+                if (BF16OUT) {
+                    if (ACC) v += (float)*reinterpret_cast<__bf16 *>(p);
+                    *reinterpret_cast<__bf16 *>(p) = (__bf16)v;
+                } else {
+                    if (ACC) v += *reinterpret_cast<float *>(p);
+                    *reinterpret_cast<float *>(p) = v;
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+}
+
 template <bool BF16OUT, bool ACC, int GMODE>
-__global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(GemmArgs g, int tiles_m, int tiles_n,
-                                                                   const GroupedArgs gr)
+__global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmArgs g, int tiles_m, int tiles_n,
+                                                                          const GroupedArgs gr)
 {
     using F = Fmt<kFmtFp4Block2D>;
     constexpr int RB = F::kRowBytes;                // 64
+    constexpr int kDma = kDmaPerTile;               // 9
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];
+    __shared__ int32_t pad_start[GMODE == 0 ? 1 : kMaxSegs + 1];
+    __shared__ int32_t tile_start[GMODE == 1 ? kMaxSegs + 1 : 1];
 
-    int tm, tn;
-    if (GMODE == 0) {
-        int64_t tm64, tn64;
-        tile_coords(tiles_m, tiles_n, tm64, tn64);
-        tm = (int)tm64; tn = (int)tn64;
-    } else {
-        // per-expert tables: padded start rows, and (ragged M) prefix of row tiles
-        __shared__ int32_t pad_start[kMaxSegs + 1];
-        __shared__ int32_t tile_start[kMaxSegs + 1];
+    uint32_t total = (uint32_t)(tiles_m * tiles_n);
+    if (GMODE != 0) {
         const int64_t *off = gr.seg_offsets;
         if ((threadIdx.x >> 6) == 0) {
             wave_prefix(gr.nseg, [&](int i) { return (int32_t)((off[i + 1] - off[i] + 127) / 128 * 128); }, pad_start);
@@ -344,78 +472,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(GemmArgs g, i
                 wave_prefix(gr.nseg, [&](int i) { return (int32_t)((off[i + 1] - off[i] + BM2 - 1) / BM2); }, tile_start);
         }
         __syncthreads();
-        const int u = blockIdx.x;
-        int e;
-        const int esize = BF16OUT ? 2 : 4;
-        if (GMODE == 1) {
-            const int rt = u / tiles_n;
-            tn = u - rt * tiles_n;
-            if (rt >= tile_start[gr.nseg]) return;
-            e = seg_search(tile_start, gr.nseg, rt);
-            tm = rt - tile_start[e];
-            const int64_t p_e = pad_start[e];
-            g.a += p_e * g.lda;
-            g.sa += (p_e / 32) * g.ldsa;
-            g.M = off[e + 1] - off[e];
-            g.c = reinterpret_cast<uint8_t *>(g.c) + off[e] * g.ldc * esize;
-            if (gr.b_group_rows) {
-                g.b += (int64_t)e * gr.b_group_rows * g.ldb;
-                g.sb += ((int64_t)e * gr.b_group_rows / 32) * g.ldsb;
-            } else {
-                g.b += (int64_t)e * gr.b_group_k / 2;
-                g.sb += (int64_t)e * gr.b_group_k / 32;
-            }
-        } else {
-            const int per = tiles_m * tiles_n;
-            e = u / per;
-            const int rest = u - e * per;
-            tm = rest / tiles_n;
-            tn = rest - tm * tiles_n;
-            const int64_t p_e = pad_start[e];
-            g.a += p_e / 2;
-            g.sa += p_e / 32;
-            g.b += p_e / 2;
-            g.sb += p_e / 32;
-            g.K = pad_start[e + 1] - p_e;
-            g.c = reinterpret_cast<uint8_t *>(g.c) + (int64_t)e * g.M * g.ldc * esize;
-        }
+        if (GMODE == 1) total = (uint32_t)__builtin_amdgcn_readfirstlane(tile_start[gr.nseg]) * (uint32_t)tiles_n;
+        else total = (uint32_t)(gr.nseg * tiles_m * tiles_n);
     }
-    const int64_t m0 = (int64_t)tm * BM2, n0 = (int64_t)tn * BN2;
+    const uint32_t nb = (uint32_t)(tiles_m * tiles_n);
+    const TileSpace<GMODE, BF16OUT> ts{g, gr, tiles_m, tiles_n, pad_start, tile_start, total,
+                                       nb / kXcds, nb % kXcds, (uint32_t)(kGroupM * tiles_n)};
+
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
     const int half = lane >> 5;
-    const uint32_t nk = (uint32_t)(g.K / BK);
-
-    // DMA j of this wave fills bytes [(4j + wave) * 1024, +1024) of an operand
-    // stage: rows 16 (4j + wave) + lane / 4, physical chunk lane % 4.
-    uint32_t offA[4], offB[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int row = 16 * (4 * j + wave) + (lane >> 2);
-        const int c = (lane & 3) ^ F::swz(row);
-        int64_t ra = m0 + row; ra = ra < g.M ? ra : g.M - 1;
-        int64_t rb = n0 + row; rb = rb < g.N ? rb : g.N - 1;
-        offA[j] = (uint32_t)(ra * g.lda + c * 16);
-        offB[j] = (uint32_t)(rb * g.ldb + c * 16);
-    }
-    // scale words: lanes 0-3 the wave's four A block rows, lanes 4-7 its four B block rows
-    const uint8_t *srcS;
-    {
-        const int q = lane & 7;
-        if (q < 4) {
-            int64_t ra = m0 + wm * 128 + q * 32; ra = ra < g.M ? ra : g.M - 1;
-            srcS = g.sa + (ra >> 5) * g.ldsa;
-        } else {
-            int64_t rb = n0 + wn * 128 + (q - 4) * 32; rb = rb < g.N ? rb : g.N - 1;
-            srcS = g.sb + (rb >> 5) * g.ldsb;
-        }
-    }
-    const uint32_t lds0 = (uint32_t)(uintptr_t)&smem[0];
-
-    const int sw = F::swz(lane & 31);
-    const int rd_a = (wm * 128 + (lane & 31)) * RB;
-    const int rd_b = kCodeBytes + (wn * 128 + (lane & 31)) * RB;
+    const int esize = BF16OUT ? 2 : 4;
+    const uint32_t ldc_bytes = (uint32_t)(g.ldc * esize);
 
     v16f acc[4][4];
 #pragma unroll
@@ -425,18 +494,84 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(GemmArgs g, i
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    // operand fragments of one K-substep (64 K values): 4 A and 4 B tiles
+    auto store = [&](const TileRef &t) __attribute__((always_inline)) {
+        const int r0 = t.m0 + wm * 128, c0 = t.n0 + wn * 128;
+        uint8_t *cb = t.c + (int64_t)r0 * ldc_bytes + (int64_t)c0 * esize;
+        if (t.m0 + BM2 <= t.M && t.n0 + BN2 <= t.N)
+            store_block<BF16OUT, ACC, false>(acc, cb, ldc_bytes, 128, 128);
+        else
+            store_block<BF16OUT, ACC, true>(acc, cb, ldc_bytes, t.M - r0, t.N - c0);
+    };
+
+    // ragged K: experts without rows give zero tiles (unchanged when accumulating)
+    if (GMODE == 2 && !ACC) {
+        for (uint32_t u = blockIdx.x; u < total; u += gridDim.x)
+            if (ts.nk_of(u) == 0) store(ts.ref(u));
+    }
+
+    uint32_t cu = ts.valid_from(blockIdx.x);        // tile being computed
+    if (cu >= total) return;
+
+    // per-lane load geometry: DMA j of this wave fills bytes [(4j + wave) * 1024,
+    // +1024) of an operand stage: rows 16 (4j + wave) + lane / 4, physical chunk
+    // lane % 4 (XOR-swizzled)
+    int row[4], c16[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        row[j] = 16 * (4 * j + wave) + (lane >> 2);
+        c16[j] = ((lane & 3) ^ F::swz(row[j])) * 16;
+    }
+    const int sq = lane & 7;                        // scale words: 0-3 A block rows, 4-7 B block rows
+    const int srow = sq < 4 ? wm * 128 + sq * 32 : wn * 128 + (sq - 4) * 32;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)&smem[0];
+
+    // load cursor: tile lu (lt), K-tile lk; past the last tile it stays on the
+    // last K-tile, whose loads then fill a stage that is never read.  The
+    // per-lane byte offsets of the tile's rows (and the scale-word source) are
+    // set when the cursor enters a tile.
+    uint32_t lu = cu, lk = 0;
+    TileRef lt = ts.ref(cu);
+    TileRef ct = lt;
+    uint32_t offA[4], offB[4];
+    const uint8_t *lsrc;
+    auto enter = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            int ra = lt.m0 + row[j]; ra = ra < lt.M ? ra : lt.M - 1;
+            int rb = lt.n0 + row[j]; rb = rb < lt.N ? rb : lt.N - 1;
+            offA[j] = (uint32_t)ra * (uint32_t)g.lda + c16[j];
+            offB[j] = (uint32_t)rb * (uint32_t)g.ldb + c16[j];
+        }
+        const bool isA = sq < 4;
+        const int lim = isA ? lt.M : lt.N;
+        int r = (isA ? lt.m0 : lt.n0) + srow; r = r < lim ? r : lim - 1;
+        lsrc = (isA ? lt.sa : lt.sb) + (uint32_t)(r >> 5) * (uint32_t)(isA ? g.ldsa : g.ldsb);
+    };
+    enter();
+    auto advance = [&]() __attribute__((always_inline)) {
+        if (++lk < lt.nk) return;
+        const uint32_t v = ts.valid_from(lu + gridDim.x);
+        if (v < total) { lu = v; lt = ts.ref(v); lk = 0; enter(); }
+        else lk = lt.nk - 1;
+    };
+    // load k (0..8) of the cursor's K-tile into ring stage `slot`:
+    //   k = 0..3 A rows 16 (4k + wave) + ..., 4..7 B likewise, 8 the scale words
+    auto load = [&](uint32_t slot, int k) __attribute__((always_inline)) {
+        const uint32_t stage = lds0 + (slot % kStages) * kStageBytes;
+        if (k < 4)
+            lds_dma16(lt.a + lk * RB, offA[k], stage + (4 * k + wave) * 1024);
+        else if (k < 8)
+            lds_dma16(lt.b + lk * RB, offB[k - 4], stage + kCodeBytes + (4 * (k - 4) + wave) * 1024);
+        else
+            lds_dma4(lsrc + lk * 4, stage + 2 * kCodeBytes + wave * 256);
+    };
+
+    const int sw = F::swz(lane & 31);
+    const int rd_a = (wm * 128 + (lane & 31)) * RB;
+    const int rd_b = kCodeBytes + (wn * 128 + (lane & 31)) * RB;
     uint4 fa0[4], fb0[4], fa1[4], fb1[4];
     uint32_t scA[4], scB[4], nA[4], nB[4];
 
-    // Pipeline.  Iteration kt: (A) the 16 MFMAs of K-substep 0 of tile kt run
-    // while the fragments of substep 1 are read; (B) once tile kt+1 has landed
-    // (vmcnt + barrier; the stage of tile kt is then free because every wave
-    // holds it in registers) the 16 MFMAs of substep 1 run while the stage of
-    // tile kt is refilled with tile kt + kStages and the first substep of tile
-    // kt+1 is read.  DMA issues and LDS reads sit between MFMAs
-    // (sched_barrier pins the order) so that the texture and LDS queues never
-    // hold the wave while the matrix core starves.
 #define Q2D_MFMA(fa, fb, scA_, scB_, ks, i, j)                                                          \
     do {                                                                                             \
         const v8i av_ = {(int)fa[i].x, (int)fa[i].y, (int)fa[i].z, (int)fa[i].w, 0, 0, 0, 0};       \
@@ -453,46 +588,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(GemmArgs g, i
         dstB[i] = *reinterpret_cast<const uint4 *>((st) + rd_b + (i) * 32 * RB + cofs_);            \
     } while (0)
 
-    // K-tile t into stage t % kStages; past the last K-tile re-read the last one
-    auto dma_addr = [&](uint32_t t, const uint8_t *&ba, const uint8_t *&bb, const uint8_t *&bs, uint32_t &stage) {
-        const uint32_t tt = t < nk ? t : nk - 1;
-        stage = lds0 + (t % kStages) * kStageBytes;
-        ba = g.a + tt * RB;
-        bb = g.b + tt * RB;
-        bs = srcS + tt * 4;
-    };
-
-    // Each K-tile's nine loads are split: the first five (A0, B0, A1, B1, scale
-    // words) go out in phase B of the iteration that frees its stage, the last
-    // four (A2, B2, A3, B3) in phase A of the next iteration.  The prologue
-    // issues tiles 0 .. kStages-2 whole and the first part of tile kStages-1.
-    auto dma_first = [&](uint32_t t, int part) {        // part 0..4
-        const uint8_t *ba, *bb, *bs;
-        uint32_t stage;
-        dma_addr(t, ba, bb, bs, stage);
-        if (part < 4) {
-            const int jj = part >> 1;
-            if ((part & 1) == 0) lds_dma16(ba, offA[jj], stage + (4 * jj + wave) * 1024);
-            else lds_dma16(bb, offB[jj], stage + kCodeBytes + (4 * jj + wave) * 1024);
-        } else {
-            lds_dma4(bs, stage + 2 * kCodeBytes + wave * 256);
-        }
-    };
-    auto dma_second = [&](uint32_t t, int part) {       // part 0..3
-        const uint8_t *ba, *bb, *bs;
-        uint32_t stage;
-        dma_addr(t, ba, bb, bs, stage);
-        const int jj = 2 + (part >> 1);
-        if ((part & 1) == 0) lds_dma16(ba, offA[jj], stage + (4 * jj + wave) * 1024);
-        else lds_dma16(bb, offB[jj], stage + kCodeBytes + (4 * jj + wave) * 1024);
-    };
-    if (nk > 0) {
-    for (int t = 0; t < kStages; ++t) {
-        for (int p = 0; p < 5; ++p) dma_first((uint32_t)t, p);
-        if (t < kStages - 1)
-            for (int p = 0; p < 4; ++p) dma_second((uint32_t)t, p);
+    // prologue: K-steps 0 .. kStages-1 (the cursor stays on step kStages-1)
+    for (uint32_t s = 0; s < kStages; ++s) {
+        if (s > 0) advance();
+        for (int k = 0; k < kDma; ++k) load(s, k);
     }
-    wait_vmcnt<(kStages - 2) * kDmaPerTile + 5>();
+    wait_vmcnt<(kStages - 1) * kDma>();
     block_barrier();
     {
         const uint4 wA = *reinterpret_cast<const uint4 *>(smem + 2 * kCodeBytes + wave * 256);
@@ -503,10 +604,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(GemmArgs g, i
         for (int i = 0; i < 4; ++i) Q2D_READ(fa0, fb0, smem, 0, i);
     }
 
-    for (uint32_t kt = 0; kt < nk; ++kt) {
-        const uint8_t *st = smem + (kt % kStages) * kStageBytes;
-        // ---- phase A: substep 0 MFMAs; substep 1 reads and the last four loads
-        // of tile kt + kStages - 1 in between
+    uint32_t s = 0;                                 // ring step
+    for (;;) {
+    for (uint32_t ck = 0; ck < ct.nk; ++ck, ++s) {
+        // the cursor moves to step s + kStages first: its (rare) switch to the
+        // next tile then precedes, rather than splits, the pipelined body
+        advance();
+        const uint8_t *st = smem + (s % kStages) * kStageBytes;
+        // ---- phase A: substep 0 MFMAs; substep 1 reads
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -517,35 +622,32 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(GemmArgs g, i
                     Q2D_READ(fa1, fb1, st, 1, i);
                     __builtin_amdgcn_sched_barrier(0);
                 }
-                if (j == 3) {
-                    dma_second(kt + kStages - 1, i);
-                    __builtin_amdgcn_sched_barrier(0);
-                }
             }
         }
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        wait_vmcnt<(kStages - 2) * kDmaPerTile>();
+        __builtin_amdgcn_s_waitcnt(0xC07F);       // lgkmcnt(0)
+        wait_vmcnt<(kStages - 2) * kDma>();
         block_barrier();
-        // ---- phase B: substep 1 MFMAs; first five loads of tile kt + kStages
-        // into the stage of tile kt; reads of substep 0 of tile kt+1
-        const uint8_t *sn = smem + ((kt + 1) % kStages) * kStageBytes;
+        // ---- phase B: substep 1 MFMAs; the nine loads of step s + kStages into
+        // the stage of step s; substep 0 reads of step s + 1
+        const uint8_t *sn = smem + ((s + 1) % kStages) * kStageBytes;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 Q2D_MFMA(fa1, fb1, scA, scB, 1, i, j);
                 __builtin_amdgcn_sched_barrier(0);
+                // loads at q = 0, 2, 4, 6, 8, 10..13; fragment reads at q = 1, 3,
+                // 5, 7 (past the last step they are unused); scale words at q = 9
                 const int q = 4 * i + j;           // 0..15
-                if (q % 3 == 0 && q / 3 < 5) {
-                    dma_first(kt + kStages, q / 3);
-                } else if (q == 7) {
+                if (q < 8 && (q & 1)) {
+                    Q2D_READ(fa0, fb0, sn, 0, q >> 1);
+                } else if (q == 9) {
                     const uint4 wA = *reinterpret_cast<const uint4 *>(sn + 2 * kCodeBytes + wave * 256);
                     const uint4 wB = *reinterpret_cast<const uint4 *>(sn + 2 * kCodeBytes + wave * 256 + 16);
                     nA[0] = wA.x; nA[1] = wA.y; nA[2] = wA.z; nA[3] = wA.w;
                     nB[0] = wB.x; nB[1] = wB.y; nB[2] = wB.z; nB[3] = wB.w;
-                } else if (q == 8 || q == 10 || q == 11 || q == 13) {
-                    const int ii = q == 8 ? 0 : q == 10 ? 1 : q == 11 ? 2 : 3;
-                    Q2D_READ(fa0, fb0, sn, 0, ii);  // past the last tile these reads are unused
+                } else if (q < 14) {
+                    load(s + kStages, q < 9 ? q >> 1 : q - 5);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -553,20 +655,22 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_256_kernel(GemmArgs g, i
 #pragma unroll
         for (int i = 0; i < 4; ++i) { scA[i] = nA[i]; scB[i] = nB[i]; }
     }
+        // ---- the tile is complete: write it and go on with the next one, whose
+        // first K-tiles are already in the ring and first fragments in registers
+        store(ct);
+        cu = ts.valid_from(cu + gridDim.x);
+        if (cu >= total) break;
+        ct = ts.ref(cu);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    }
     wait_vmcnt<0>();
-    }   // nk > 0
 #undef Q2D_MFMA
 #undef Q2D_READ
-
-    // ---- epilogue.  Lane holds column (lane % 32) of each 32-column tile j and
-    // rows 8 (r / 4) + 4 (lane / 32) + r % 4 of each 32-row tile i.
-    const int64_t row0 = m0 + wm * 128 + 4 * half;
-    const int64_t col0 = n0 + wn * 128 + (lane & 31);
-    if (m0 + BM2 <= g.M && n0 + BN2 <= g.N) {
-        store_tile<BF16OUT, ACC, false>(acc, g, row0, col0);
-    } else {
-        store_tile<BF16OUT, ACC, true>(acc, g, row0, col0);
-    }
 }
 
 // Large-tile MXFP8 kernel (the query/key projections): 256 x 256 output tile,
@@ -720,13 +824,33 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
     }
 }
 
-template <bool BF, int GMODE>
-hipError_t launch_256(const GemmArgs &g, const GroupedArgs &gr, int tm, int tn, int grid, hipStream_t s)
+// compute units of the current device (queried once per device)
+int cu_count()
 {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int n = cache[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cache[dev].store(n, std::memory_order_relaxed);
+    }
+    return n;
+}
+
+// persistent kernel over at most `tiles` tiles: one workgroup per CU, a
+// multiple of 8 (the XCD count) so that every workgroup stays on one XCD's
+// share of the tile order
+template <bool BF, int GMODE>
+hipError_t launch_persistent(const GemmArgs &g, const GroupedArgs &gr, int tm, int tn, int64_t tiles, hipStream_t s)
+{
+    int64_t grid = cu_count();
+    grid = grid < tiles ? grid : tiles;
+    grid = (grid + kXcds - 1) / kXcds * kXcds;
     if (g.accumulate)
-        hipLaunchKernelGGL((gemm_fp4_256_kernel<BF, true, GMODE>), dim3((unsigned)grid), dim3(kThreads), 0, s, g, tm, tn, gr);
+        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<BF, true, GMODE>), dim3((unsigned)grid), dim3(kThreads), 0, s, g, tm, tn, gr);
     else
-        hipLaunchKernelGGL((gemm_fp4_256_kernel<BF, false, GMODE>), dim3((unsigned)grid), dim3(kThreads), 0, s, g, tm, tn, gr);
+        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<BF, false, GMODE>), dim3((unsigned)grid), dim3(kThreads), 0, s, g, tm, tn, gr);
     return hipGetLastError();
 }
 
@@ -748,8 +872,8 @@ hipError_t launch_gemm(const GemmArgs &g, int fmt, int c_is_bf16, hipStream_t st
     if (fmt == kFmtFp4Block2D && off32 && ((g.M + BM2 - 1) / BM2) * ((g.N + BN2 - 1) / BN2) >= 128) {
         const int tm = (int)((g.M + BM2 - 1) / BM2), tn = (int)((g.N + BN2 - 1) / BN2);
         const GroupedArgs none = {nullptr, 0, 0, 0, 0, 0};
-        return c_is_bf16 ? launch_256<true, 0>(g, none, tm, tn, tm * tn, stream)
-                         : launch_256<false, 0>(g, none, tm, tn, tm * tn, stream);
+        return c_is_bf16 ? launch_persistent<true, 0>(g, none, tm, tn, (int64_t)tm * tn, stream)
+                         : launch_persistent<false, 0>(g, none, tm, tn, (int64_t)tm * tn, stream);
     }
     if (fmt == kFmtFp4Block2D)
         return c_is_bf16 ? launch_t<kFmtFp4Block2D, true>(g, stream) : launch_t<kFmtFp4Block2D, false>(g, stream);
@@ -773,12 +897,12 @@ hipError_t launch_grouped_gemm(const GemmArgs &g, const GroupedArgs &gr, int c_i
     if (!gr.ragged_k) {
         // row tiles over all experts: at most total_rows / 256 + nseg
         const int rt = (int)((gr.total_rows + BM2 - 1) / BM2) + gr.nseg;
-        return c_is_bf16 ? launch_256<true, 1>(g, gr, 0, tn, rt * tn, stream)
-                         : launch_256<false, 1>(g, gr, 0, tn, rt * tn, stream);
+        return c_is_bf16 ? launch_persistent<true, 1>(g, gr, 0, tn, (int64_t)rt * tn, stream)
+                         : launch_persistent<false, 1>(g, gr, 0, tn, (int64_t)rt * tn, stream);
     }
     const int tm = (int)((g.M + BM2 - 1) / BM2);
-    return c_is_bf16 ? launch_256<true, 2>(g, gr, tm, tn, gr.nseg * tm * tn, stream)
-                     : launch_256<false, 2>(g, gr, tm, tn, gr.nseg * tm * tn, stream);
+    return c_is_bf16 ? launch_persistent<true, 2>(g, gr, tm, tn, (int64_t)gr.nseg * tm * tn, stream)
+                     : launch_persistent<false, 2>(g, gr, tm, tn, (int64_t)gr.nseg * tm * tn, stream);
 }
 
 }  // namespace q2d

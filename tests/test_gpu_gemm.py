@@ -70,6 +70,32 @@ def test_gemm_fp4(q2d, M, N, K, ta, tb):
     check_bf16(c16, ref)
 
 
+# More output tiles than the device has CUs, so every workgroup of the
+# persistent kernel walks several tiles; K of 1, 3 and 5 K-tiles (fewer than,
+# and more than, the LDS ring's four stages, so one tile's loads run into the
+# next tile's) and ragged M and N edges.
+MULTI_TILE_SHAPES = [(4200, 4100, 128), (4100, 4200, 384), (6000, 3000, 640)]
+
+
+@pytest.mark.parametrize("M,N,K", MULTI_TILE_SHAPES)
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 1)])
+def test_gemm_fp4_multi_tile_per_workgroup(q2d, M, N, K, ta, tb):
+    a_shape = (K, M) if ta else (M, K)
+    b_shape = (K, N) if tb else (N, K)
+    A = synth.normal(a_shape, 1.0, 7 * M + K, torch.bfloat16, device=DEV)
+    B = synth.normal(b_shape, 0.02, 7 * N + K + 1, torch.bfloat16, device=DEV)
+    qa, oa = quant(q2d, A, "rtn")
+    qb, ob = quant(q2d, B, "sr", 3, 0)
+    ref = oracle.gemm(oracle.operand(oa, bool(ta)), oracle.operand(ob, bool(tb)))
+    c32 = q2d.q2d_gemm(qa, ta, qb, tb, out_dtype=torch.float32)
+    assert rel_frob(c32.cpu().numpy(), ref) <= TOL
+    # bf16 output accumulated onto an existing C
+    c0 = synth.normal((M, N), 0.5, 11, torch.bfloat16, device=DEV)
+    c16 = c0.clone()
+    q2d.q2d_gemm(qa, ta, qb, tb, out=c16, accumulate=True)
+    check_bf16(c16, ref + c0.float().cpu().numpy().astype(np.float64))
+
+
 def test_gemm_accumulate_and_ldc(q2d):
     A = synth.normal((200, 320), 1.0, 1, torch.bfloat16, device=DEV)
     B = synth.normal((150, 320), 1.0, 2, torch.bfloat16, device=DEV)
