@@ -13,6 +13,9 @@ What each function follows:
   * ``gemm``: Y = X W^T, dX = dY W, dW = dY^T X on quantized operands
     (Sec. 3, "Application to linear layers"; App. C);
   * ``quantize_mxfp8``: MXFP8 for the query/key projections (Sec. 3.2; App. C);
+  * ``quantize_fp4_1d``: 1D FP4 for activations, 1x32 blocks for the forward
+    copy and 32x1 blocks for the weight-gradient copy (Sec. 3, "Application to
+    linear layers"; App. C, "Activations");
   * ``quantize_fp4_grouped``: each expert's row segment is its own matrix
     (the MoE setting of Sec. 4.1) with boundary blocks over valid rows only
     (App. D).
@@ -66,6 +69,8 @@ def lib():
                                          P, I64, P, I64, P, I64, P, I64, I32]
         L.or_quantize_mxfp8.argtypes = [P, I32, I64, I64, I64, I64,
                                         P, I64, P, I64, P, I64, P, I64, I32]
+        L.or_quantize_fp4_1d.argtypes = [P, I32, I64, I64, I64, I64, I32, U64, U64,
+                                         P, I64, P, I64, P, I64, P, I64, I32]
         L.or_fp4_codes.argtypes = [P, P, P, I32, I64, P]
         L.or_e4m3_codes.argtypes = [P, P, I64, P]
         L.or_max_threads.restype = I32
@@ -150,6 +155,17 @@ def mxfp8_layout(R: int, C: int) -> dict:
         "codes": (R, _rup(C, 128)),
         "scales": (R, _rup(C, 128) // 32),
         "codes_t": (C, _rup(R, 128)),
+        "scales_t": (C, _rup(R, 128) // 32),
+    }
+
+
+def fp4_1d_layout(R: int, C: int) -> dict:
+    """1D FP4: codes packed as for 2D blocks, one scale per row (per column for
+    the transposed copy) and 32-element K-group."""
+    return {
+        "codes": (R, _rup(C, 128) // 2),
+        "scales": (R, _rup(C, 128) // 32),
+        "codes_t": (C, _rup(R, 128) // 2),
         "scales_t": (C, _rup(R, 128) // 32),
     }
 
@@ -283,6 +299,23 @@ def quantize_mxfp8(x, threads: int = 0) -> dict:
     return out
 
 
+def quantize_fp4_1d(x, mode: str = "rtn", seed: int = 0, offset: int = 0, threads: int = 0) -> dict:
+    """1D FP4: rowwise 1x32 copy (codes/scales) and colwise 32x1 copy stored
+    transposed (codes_t/scales_t); truncation-free scales, E2M1 codes, the
+    element's one stochastic draw used in both copies."""
+    hold, ptr, dt, R, C, sr, sc = _as_input(x)
+    lay = fp4_1d_layout(R, C)
+    out = {k: np.zeros(v, dtype=np.uint8) for k, v in lay.items()}
+    lib().or_quantize_fp4_1d(ptr, dt, R, C, sr, sc, 1 if mode == "sr" else 0,
+                             int(seed), int(offset),
+                             out["codes"].ctypes.data, lay["codes"][1],
+                             out["scales"].ctypes.data, lay["scales"][1],
+                             out["codes_t"].ctypes.data, lay["codes_t"][1],
+                             out["scales_t"].ctypes.data, lay["scales_t"][1], int(threads))
+    out["rows"], out["cols"] = R, C
+    return out
+
+
 # ------------------------------------------------------------------ dequantization
 
 def _scale_values(sbytes: np.ndarray) -> np.ndarray:
@@ -314,6 +347,13 @@ def dequant_fp4(codes: np.ndarray, scales: np.ndarray, R: int, C: int) -> np.nda
     return q * s[rb][:, cb]
 
 
+def dequant_fp4_1d(codes: np.ndarray, scales: np.ndarray, R: int, C: int) -> np.ndarray:
+    """R x C float64 values of a 1x32-block FP4 operand (row r, K index c)."""
+    q = fp4_values(_unpack(codes[:R], C))
+    s = _scale_values(scales[:R])
+    return q * s[:, np.arange(C) // 32]
+
+
 def dequant_mxfp8(codes: np.ndarray, scales: np.ndarray, R: int, C: int) -> np.ndarray:
     """R x C float64 values of a 1x32-block E4M3 operand (K index along columns)."""
     b = codes[:R, :C].astype(np.int64)
@@ -334,6 +374,10 @@ def operand(q: dict, transpose: bool, fmt: str = "fp4") -> np.ndarray:
         if not transpose:
             return dequant_fp4(q["codes"], q["scales"], R, C)
         return dequant_fp4(q["codes_t"], q["scales_t"], C, R)
+    if fmt == "fp4_1d":
+        if not transpose:
+            return dequant_fp4_1d(q["codes"], q["scales"], R, C)
+        return dequant_fp4_1d(q["codes_t"], q["scales_t"], C, R)
     if not transpose:
         return dequant_mxfp8(q["codes"], q["scales"], R, C)
     return dequant_mxfp8(q["codes_t"], q["scales_t"], C, R)
@@ -344,13 +388,16 @@ def gemm(a: np.ndarray, b: np.ndarray) -> np.ndarray:
     return np.asarray(a, dtype=np.float64) @ np.asarray(b, dtype=np.float64).T
 
 
-def linear(qx: dict, qw: dict, qdy: dict, fmt: str = "fp4") -> dict:
+def linear(qx: dict, qw: dict, qdy: dict, fmt: str = "fp4", fmt_x: str | None = None) -> dict:
     """The three GEMMs of a linear layer on quantized operands (App. C):
-    Y = X W^T, dX = dY W, dW = dY^T X, each operand quantized once."""
-    X = operand(qx, False, fmt)
+    Y = X W^T, dX = dY W, dW = dY^T X, each operand quantized once.  fmt_x
+    (default fmt) is the format of X: "fp4_1d" for the paper's activation
+    placement (App. C, "Activations")."""
+    fx = fmt if fmt_x is None else fmt_x
+    X = operand(qx, False, fx)
     W = operand(qw, False, fmt)
     dY = operand(qdy, False, fmt)
-    Xt = operand(qx, True, fmt)
+    Xt = operand(qx, True, fx)
     Wt = operand(qw, True, fmt)
     dYt = operand(qdy, True, fmt)
     return {"Y": gemm(X, W), "dX": gemm(dY, Wt), "dW": gemm(dYt, Xt)}

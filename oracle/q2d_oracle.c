@@ -18,6 +18,8 @@
  *     gradients (Sec. 3.1; App. E).
  *   - MXFP8 for the Q/K path (Sec. 3.2; App. C): 1x32 blocks, E4M3 elements,
  *     the same truncation-free rule with Qp = 448.
+ *   - 1D FP4 for activations (Sec. 3; App. C): 1x32 and 32x1 blocks with the
+ *     FP4 scale rule and codec.
  *
  * Readings of what the paper leaves open (each is listed in the design notes):
  *   - the FP4 grid is OCP E2M1, magnitudes {0, .5, 1, 1.5, 2, 3, 4, 6};
@@ -214,6 +216,83 @@ void or_quantize_fp4_2d(const void *x, int dtype, int64_t R, int64_t C, int64_t 
                     if (codes) put_nibble(codes + r * ldc, c, code);
                     if (codes_t) put_nibble(codes_t + c * ldt, r, code);
                 }
+        }
+    }
+}
+
+/* ---------------------------------------------------------------- 1D FP4 */
+
+/*
+ * One-dimensional FP4 for activations (Sec. 3, "Application to linear
+ * layers": activations keep a 1D block layout; App. C, "Activations"; the
+ * 1D-FP4 activation entry of the training configuration table).  The block is
+ * a 1 x 32 run of one row for the copy the forward GEMM reads (K = columns),
+ * and a 32 x 1 run of one column for the copy the weight-gradient GEMM reads
+ * (K = rows) -- the forward/backward scale mismatch of 1D layouts that the
+ * 2D blocks remove (Sec. 2, "Scale inconsistency under transposition").  Each
+ * block gets the truncation-free E8M0 scale of the 2D method (Sec. 3.1) and its
+ * elements the same E2M1 codec; a stochastic element uses its one storage-index
+ * draw in both copies.
+ *   rowwise: codes [R][ldc] (byte (r, c/2), low nibble = even c), scales [R][lds]
+ *            (entry (r, c/32));
+ *   colwise: codes_t [C][ldt] (byte (c, r/2), low nibble = even r),
+ *            scales_t [C][ldst] (entry (c, r/32)).
+ */
+void or_quantize_fp4_1d(const void *x, int dtype, int64_t R, int64_t C, int64_t sr, int64_t sc,
+                        int mode, uint64_t seed, uint64_t offset,
+                        uint8_t *codes, int64_t ldc, uint8_t *scales, int64_t lds,
+                        uint8_t *codes_t, int64_t ldt, uint8_t *scales_t, int64_t ldst,
+                        int nthreads)
+{
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(static)
+#endif
+    for (int64_t r = 0; r < R; ++r) {                 /* rowwise: 1 x 32 blocks */
+        if (!codes) continue;
+        for (int64_t J = 0; J * 32 < C; ++J) {
+            int64_t c1 = (J + 1) * 32 < C ? (J + 1) * 32 : C;
+            double M = 0.0; int finite = 1;
+            for (int64_t c = J * 32; c < c1; ++c) {
+                double v = load(x, dtype, r * sr + c * sc);
+                if (!isfinite(v)) finite = 0; else if (fabs(v) > M) M = fabs(v);
+            }
+            int e = or_fp4_scale_exponent(M);
+            scales[r * lds + J] = finite ? (uint8_t)(e + 127) : 0xFF;
+            for (int64_t c = J * 32; c < c1; ++c) {
+                unsigned code = 0;
+                if (finite) {
+                    int64_t idx = r * sr + c * sc;
+                    uint32_t r16 = mode ? or_sr_bits(idx, seed, offset) : 0;
+                    code = or_fp4_code(load(x, dtype, idx), e, mode, r16);
+                }
+                put_nibble(codes + r * ldc, c, code);
+            }
+        }
+    }
+#ifdef _OPENMP
+#pragma omp parallel for schedule(static)
+#endif
+    for (int64_t c = 0; c < C; ++c) {                 /* colwise: 32 x 1 blocks */
+        if (!codes_t) continue;
+        for (int64_t I = 0; I * 32 < R; ++I) {
+            int64_t r1 = (I + 1) * 32 < R ? (I + 1) * 32 : R;
+            double M = 0.0; int finite = 1;
+            for (int64_t r = I * 32; r < r1; ++r) {
+                double v = load(x, dtype, r * sr + c * sc);
+                if (!isfinite(v)) finite = 0; else if (fabs(v) > M) M = fabs(v);
+            }
+            int e = or_fp4_scale_exponent(M);
+            scales_t[c * ldst + I] = finite ? (uint8_t)(e + 127) : 0xFF;
+            for (int64_t r = I * 32; r < r1; ++r) {
+                unsigned code = 0;
+                if (finite) {
+                    int64_t idx = r * sr + c * sc;
+                    uint32_t r16 = mode ? or_sr_bits(idx, seed, offset) : 0;
+                    code = or_fp4_code(load(x, dtype, idx), e, mode, r16);
+                }
+                put_nibble(codes_t + c * ldt, r, code);
+            }
         }
     }
 }
