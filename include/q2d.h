@@ -60,7 +60,9 @@ typedef enum {
 
 typedef enum {
     Q2D_FMT_FP4_2D = 0,      /* E2M1 codes, one E8M0 scale per 32x32 block (Sec. 3) */
-    Q2D_FMT_MXFP8 = 1        /* E4M3 codes, one E8M0 scale per 1x32 block (Sec. 3.2) */
+    Q2D_FMT_MXFP8 = 1,       /* E4M3 codes, one E8M0 scale per 1x32 block (Sec. 3.2) */
+    Q2D_FMT_FP4_1D = 2       /* E2M1 codes, one E8M0 scale per 1x32 block: activations
+                                (Sec. 3, "Application to linear layers"; App. C) */
 } q2d_fmt;
 
 /*
@@ -86,6 +88,17 @@ typedef enum {
  *            Unlike FP4_2D, the two copies have different scales.
  *   Rows are padded to multiples of 128 bytes (codes) / 4 bytes (scales) as
  *   for FP4_2D, padding 0.
+ *
+ * FP4_1D (activations; Sec. 3, "Application to linear layers"; App. C,
+ * "Activations"):
+ *   codes / codes_t packed exactly as for FP4_2D;
+ *   scales   [rows][ld_scales]: byte (r, c/32) is the scale of the 1x32 block
+ *            of row r (K = cols);
+ *   scales_t [cols][ld_scales_t]: byte (c, r/32) is the scale of the 32x1
+ *            block of column c (K = rows).
+ *   The two copies have different blocks, scales and (in general) codes: the
+ *   forward/backward inconsistency of 1D layouts (Sec. 2) that the 2D blocks
+ *   of weights and gradients avoid.
  *
  * All leading dimensions are in bytes.  Pointers may be NULL for an
  * orientation the caller does not need (codes with scales, codes_t with
@@ -137,6 +150,21 @@ q2d_status q2d_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols,
                         uint64_t seed, uint64_t offset, q2d_tensor *out, hipStream_t stream);
 
 /*
+ * 1D-block FP4 quantization of activations (Sec. 3, "Application to linear
+ * layers": activations keep a 1D layout; App. C, "Activations"): one pass
+ * writes the rowwise copy (1x32 blocks along columns; codes/scales, read by
+ * the forward GEMM) and the colwise copy (32x1 blocks along rows, stored
+ * transposed; codes_t/scales_t, read by the weight-gradient GEMM).  Every
+ * block gets the truncation-free scale and the E2M1 codec of q2d_quantize;
+ * for SR the element's one draw (same storage-index contract) serves both
+ * copies.  Arguments, alignment and errors as for q2d_quantize; out from
+ * q2d_tensor_init(FP4_1D, rows, cols, 32).
+ */
+q2d_status q2d_quantize_1d(const void *x, q2d_dtype dt, int64_t rows, int64_t cols,
+                           int64_t stride_r, int64_t stride_c, int32_t block, q2d_round mode,
+                           uint64_t seed, uint64_t offset, q2d_tensor *out, hipStream_t stream);
+
+/*
  * MXFP8 quantization for the query/key projections (Sec. 3.2; App. C):
  * E4M3 codes rounded to nearest even, one truncation-free E8M0 scale per 1x32
  * block (smallest power of two S with 448 * S >= block maximum).  The rowwise
@@ -154,7 +182,9 @@ q2d_status mxfp8_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t col
  *
  * op(X) = X (uses codes/scales; K = X.cols) when transX == 0, or X^T (uses
  * codes_t/scales_t; K = X.rows) when transX == 1.  M = rows of op(A),
- * N = rows of op(B); both must have the same K and the same fmt.
+ * N = rows of op(B); both must have the same K.  FP4_2D and FP4_1D operands
+ * may be mixed (1D activations with 2D weights and gradients: App. C); MXFP8
+ * pairs only with MXFP8.
  *   forward     Y  = X  W^T : q2d_gemm(X, 0, W, 0, ...)
  *   data grad   dX = dY W   : q2d_gemm(dY, 0, W, 1, ...)
  *   weight grad dW = dY^T X : q2d_gemm(dY, 1, X, 1, ...)
@@ -170,7 +200,9 @@ q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int tr
  * quantizes X [T][K] and W [N][K] (row-major, dtype dt) into qX and qW (both
  * orientations, kept for the backward pass) and runs the forward GEMM into
  * Y [T][N] (row-major, ldy = N, dtype y_dt).  The SR streams of X and W use
- * (seed, offset_x) and (seed, offset_w).
+ * (seed, offset_x) and (seed, offset_w).  qX may be FP4_1D (the paper's
+ * activation layout, App. C): X is then quantized with q2d_quantize_1d and the
+ * backward pass's weight gradient reads its 32x1 copy.
  */
 q2d_status q2d_linear_fwd(const void *X, const void *W, q2d_dtype dt, int64_t T, int64_t N,
                           int64_t K, q2d_round mode_x, q2d_round mode_w, uint64_t seed,

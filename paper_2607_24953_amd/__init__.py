@@ -14,8 +14,8 @@ import os
 import torch
 
 __all__ = [
-    "Q2DError", "QTensor", "RTN", "SR", "FP4_2D", "MXFP8", "lib_path",
-    "q2d_tensor_init", "q2d_quantize", "mxfp8_quantize", "q2d_gemm",
+    "Q2DError", "QTensor", "RTN", "SR", "FP4_2D", "MXFP8", "FP4_1D", "lib_path",
+    "q2d_tensor_init", "q2d_quantize", "q2d_quantize_1d", "mxfp8_quantize", "q2d_gemm",
     "q2d_linear_fwd", "q2d_linear_bwd", "q2d_grouped_tensor_init", "q2d_grouped_quantize",
     "q2d_grouped_gemm", "q2d_status_string",
 ]
@@ -24,7 +24,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 lib_path = os.path.join(_HERE, "libq2d.so")
 
 RTN, SR = 0, 1
-FP4_2D, MXFP8 = 0, 1
+FP4_2D, MXFP8, FP4_1D = 0, 1, 2
 _F32, _BF16 = 0, 1
 _ROUND = {"rtn": RTN, "sr": SR, RTN: RTN, SR: SR}
 
@@ -50,6 +50,7 @@ def _load():
     TP = ctypes.POINTER(_Tensor)
     L.q2d_tensor_init.argtypes = [TP, I32, I64, I64, I32, ctypes.POINTER(ctypes.c_int64)]
     L.q2d_quantize.argtypes = [P, I32, I64, I64, I64, I64, I32, I32, U64, U64, TP, P]
+    L.q2d_quantize_1d.argtypes = [P, I32, I64, I64, I64, I64, I32, I32, U64, U64, TP, P]
     L.mxfp8_quantize.argtypes = [P, I32, I64, I64, I64, I64, TP, P]
     L.q2d_gemm.argtypes = [TP, I32, TP, I32, P, I32, I64, I32, P]
     L.q2d_linear_fwd.argtypes = [P, P, I32, I64, I64, I64, I32, I32, U64, U64, U64, TP, TP, P, I32, P]
@@ -152,6 +153,19 @@ def q2d_quantize(x: torch.Tensor, mode="rtn", seed: int = 0, offset: int = 0,
     return out
 
 
+def q2d_quantize_1d(x: torch.Tensor, mode="rtn", seed: int = 0, offset: int = 0,
+                    out: QTensor | None = None, block: int = 32) -> QTensor:
+    """1D FP4 quantization of activations: 1x32 rowwise copy and 32x1 colwise copy."""
+    _check_input(x)
+    R, C = x.shape
+    if out is None:
+        out = QTensor(FP4_1D, R, C, x.device, block)
+    _check(_lib.q2d_quantize_1d(x.data_ptr(), _dtype_code(x.dtype), R, C, x.stride(0), x.stride(1),
+                                block, _ROUND[mode], int(seed), int(offset), out.ptr(),
+                                _stream(x.device)), "q2d_quantize_1d")
+    return out
+
+
 def mxfp8_quantize(x: torch.Tensor, out: QTensor | None = None) -> QTensor:
     """MXFP8 (E4M3, 1x32) quantization: rowwise and colwise copies in one pass."""
     _check_input(x)
@@ -180,15 +194,16 @@ def q2d_gemm(A: QTensor, transA: int, B: QTensor, transB: int, out: torch.Tensor
 
 def q2d_linear_fwd(X: torch.Tensor, W: torch.Tensor, mode_x="rtn", mode_w="rtn", seed: int = 0,
                    offset_x: int = 0, offset_w: int = 1, y_dtype=torch.bfloat16,
-                   qX: QTensor | None = None, qW: QTensor | None = None, Y=None):
-    """Y = Q(X) Q(W)^T; returns (Y, qX, qW) with both orientations kept."""
+                   qX: QTensor | None = None, qW: QTensor | None = None, Y=None, fmt_x: int = FP4_2D):
+    """Y = Q(X) Q(W)^T; returns (Y, qX, qW) with both orientations kept.  fmt_x
+    FP4_1D quantizes X in 1D blocks (the activation placement of the paper)."""
     _check_input(X)
     _check_input(W)
     T, K = X.shape
     N = W.shape[0]
     if not (X.is_contiguous() and W.is_contiguous()) or W.shape[1] != K or X.dtype != W.dtype:
         raise Q2DError("q2d_linear_fwd expects contiguous X [T,K] and W [N,K] of one dtype")
-    qX = qX or QTensor(FP4_2D, T, K, X.device)
+    qX = qX or QTensor(fmt_x, T, K, X.device)
     qW = qW or QTensor(FP4_2D, N, K, X.device)
     if Y is None:
         Y = torch.empty((T, N), dtype=y_dtype, device=X.device)

@@ -28,6 +28,11 @@ Layout layout_of(q2d_fmt fmt, int64_t R, int64_t C)
         l.ld_codes_t = rup(R, kPadK) / 2; l.rows_codes_t = C;
         l.ld_scales = rup(C, kPadK) / 32; l.rows_scales = cdiv(R, 32);
         l.ld_scales_t = rup(R, kPadK) / 32; l.rows_scales_t = cdiv(C, 32);
+    } else if (fmt == Q2D_FMT_FP4_1D) {
+        l.ld_codes = rup(C, kPadK) / 2;   l.rows_codes = R;
+        l.ld_codes_t = rup(R, kPadK) / 2; l.rows_codes_t = C;
+        l.ld_scales = rup(C, kPadK) / 32; l.rows_scales = R;
+        l.ld_scales_t = rup(R, kPadK) / 32; l.rows_scales_t = C;
     } else {
         l.ld_codes = rup(C, kPadK);       l.rows_codes = R;
         l.ld_codes_t = rup(R, kPadK);     l.rows_codes_t = C;
@@ -120,7 +125,7 @@ q2d_status q2d_tensor_init(q2d_tensor *t, q2d_fmt fmt, int64_t rows, int64_t col
                            int64_t bytes[4])
 {
     if (!t || rows <= 0 || cols <= 0) return Q2D_EINVAL;
-    if (fmt != Q2D_FMT_FP4_2D && fmt != Q2D_FMT_MXFP8) return Q2D_EINVAL;
+    if (fmt != Q2D_FMT_FP4_2D && fmt != Q2D_FMT_MXFP8 && fmt != Q2D_FMT_FP4_1D) return Q2D_EINVAL;
     if (block != 32) return Q2D_EUNSUPPORTED;
     const Layout l = layout_of(fmt, rows, cols);
     t->fmt = fmt; t->block = block; t->rows = rows; t->cols = cols;
@@ -147,7 +152,24 @@ q2d_status q2d_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols,
     s = check_tensor(out, Q2D_FMT_FP4_2D, rows, cols);
     if (s != Q2D_OK) return s;
     const QuantArgs a = make_quant_args(x, rows, cols, stride_r, stride_c, seed, offset, out);
-    if (launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, stream) != hipSuccess) return Q2D_ELAUNCH;
+    if (launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, false, stream) != hipSuccess) return Q2D_ELAUNCH;
+    return Q2D_OK;
+}
+
+q2d_status q2d_quantize_1d(const void *x, q2d_dtype dt, int64_t rows, int64_t cols, int64_t stride_r,
+                           int64_t stride_c, int32_t block, q2d_round mode, uint64_t seed, uint64_t offset,
+                           q2d_tensor *out, hipStream_t stream)
+{
+    q2d_status s = check_input(x, dt, rows, cols, stride_r, stride_c);
+    if (s != Q2D_OK) return s;
+    if (mode != Q2D_RTN && mode != Q2D_SR) return Q2D_EINVAL;
+    if (block != 32) return Q2D_EUNSUPPORTED;
+    s = check_tensor(out, Q2D_FMT_FP4_1D, rows, cols);
+    if (s != Q2D_OK) return s;
+    // a transposed view's rowwise blocks are its storage's column blocks: the
+    // swap of make_quant_args sends each copy to the right buffers
+    const QuantArgs a = make_quant_args(x, rows, cols, stride_r, stride_c, seed, offset, out);
+    if (launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, true, stream) != hipSuccess) return Q2D_ELAUNCH;
     return Q2D_OK;
 }
 
@@ -180,16 +202,20 @@ q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int tr
     if (!A || !B || !C || !valid_dtype(c_dt)) return Q2D_EINVAL;
     if ((transA != 0 && transA != 1) || (transB != 0 && transB != 1)) return Q2D_EINVAL;
     if (accumulate != 0 && accumulate != 1) return Q2D_EINVAL;
-    if (A->fmt != B->fmt || (A->fmt != Q2D_FMT_FP4_2D && A->fmt != Q2D_FMT_MXFP8)) return Q2D_EINVAL;
+    // FP4 operands may mix 2D and 1D blocks (activations); MXFP8 pairs with MXFP8
+    const bool fp4a = A->fmt == Q2D_FMT_FP4_2D || A->fmt == Q2D_FMT_FP4_1D;
+    const bool fp4b = B->fmt == Q2D_FMT_FP4_2D || B->fmt == Q2D_FMT_FP4_1D;
+    if (!(fp4a && fp4b) && !(A->fmt == Q2D_FMT_MXFP8 && B->fmt == Q2D_FMT_MXFP8)) return Q2D_EINVAL;
     if (A->block != 32 || B->block != 32) return Q2D_EUNSUPPORTED;
     if (A->rows <= 0 || A->cols <= 0 || B->rows <= 0 || B->cols <= 0) return Q2D_EINVAL;
     const int64_t M = transA ? A->cols : A->rows, Ka = transA ? A->rows : A->cols;
     const int64_t N = transB ? B->cols : B->rows, Kb = transB ? B->rows : B->cols;
     if (Ka != Kb || ldc < N) return Q2D_EINVAL;
     if (!aligned(C, (uintptr_t)dtype_bytes(c_dt))) return Q2D_EINVAL;
-    const q2d_fmt fmt = (q2d_fmt)A->fmt;
-    const Layout la = layout_of(fmt, A->rows, A->cols), lb = layout_of(fmt, B->rows, B->cols);
+    const Layout la = layout_of((q2d_fmt)A->fmt, A->rows, A->cols), lb = layout_of((q2d_fmt)B->fmt, B->rows, B->cols);
     GemmArgs g;
+    g.a1d = A->fmt == Q2D_FMT_FP4_1D;
+    g.b1d = B->fmt == Q2D_FMT_FP4_1D;
     if (!transA) {
         if (!check_pair(A->codes, A->ld_codes, la.ld_codes, A->scales, A->ld_scales, la.ld_scales) || !A->codes)
             return Q2D_EINVAL;
@@ -213,7 +239,7 @@ q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int tr
     g.c = C; g.ldc = ldc;
     g.M = M; g.N = N; g.K = rup(Ka, kPadK);
     g.accumulate = accumulate;
-    if (launch_gemm(g, fmt == Q2D_FMT_FP4_2D ? kFmtFp4Block2D : kFmtMxfp8, c_dt == Q2D_BF16, stream) != hipSuccess)
+    if (launch_gemm(g, fp4a ? kFmtFp4Block2D : kFmtMxfp8, c_dt == Q2D_BF16, stream) != hipSuccess)
         return Q2D_ELAUNCH;
     return Q2D_OK;
 }
@@ -224,7 +250,9 @@ q2d_status q2d_linear_fwd(const void *X, const void *W, q2d_dtype dt, int64_t T,
                           hipStream_t stream)
 {
     if (!qX || !qW || !qX->codes || !qW->codes) return Q2D_EINVAL;
-    q2d_status s = q2d_quantize(X, dt, T, K, K, 1, 32, mode_x, seed, offset_x, qX, stream);
+    q2d_status s = qX->fmt == Q2D_FMT_FP4_1D
+                       ? q2d_quantize_1d(X, dt, T, K, K, 1, 32, mode_x, seed, offset_x, qX, stream)
+                       : q2d_quantize(X, dt, T, K, K, 1, 32, mode_x, seed, offset_x, qX, stream);
     if (s != Q2D_OK) return s;
     s = q2d_quantize(W, dt, N, K, K, 1, 32, mode_w, seed, offset_w, qW, stream);
     if (s != Q2D_OK) return s;
@@ -271,7 +299,7 @@ q2d_status q2d_grouped_quantize(const void *x, q2d_dtype dt, int64_t rows, int64
     a.rows_pad = cap;               // grid bound over padded rows
     a.seg_offsets = seg_offsets;
     a.nseg = nseg;
-    if (launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, stream) != hipSuccess) return Q2D_ELAUNCH;
+    if (launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, false, stream) != hipSuccess) return Q2D_ELAUNCH;
     return Q2D_OK;
 }
 
@@ -289,6 +317,7 @@ q2d_status q2d_grouped_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B
     const int64_t cap = grouped_capacity(total_rows, nseg);
     const Layout la = layout_of(Q2D_FMT_FP4_2D, A->rows, A->cols), lb = layout_of(Q2D_FMT_FP4_2D, B->rows, B->cols);
     GemmArgs g;
+    g.a1d = g.b1d = 0;
     GroupedArgs gr;
     gr.seg_offsets = seg_offsets;
     gr.nseg = nseg;

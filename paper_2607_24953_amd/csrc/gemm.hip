@@ -122,8 +122,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmArgs g, int64_
     for (int i = 0; i < 2; ++i) {
         int64_t ra = m0 + wm * 64 + i * 32 + (lane & 31); ra = ra < g.M ? ra : g.M - 1;
         int64_t rb = n0 + wn * 64 + i * 32 + (lane & 31); rb = rb < g.N ? rb : g.N - 1;
-        sa_row[i] = g.sa + (ra >> F::kScaleRowShift) * g.ldsa;
-        sb_row[i] = g.sb + (rb >> F::kScaleRowShift) * g.ldsb;
+        sa_row[i] = g.sa + (ra >> (g.a1d ? 0 : F::kScaleRowShift)) * g.ldsa;
+        sb_row[i] = g.sb + (rb >> (g.b1d ? 0 : F::kScaleRowShift)) * g.ldsb;
     }
 
     v16f acc[2][2];
@@ -452,13 +452,22 @@ __device__ __forceinline__ void store_block(v16f (&acc)[4][4], uint8_t *cbase, u
         }
 }
 
-template <bool BF16OUT, bool ACC, int GMODE>
+// SM: bit 0 -- A has 1x32 blocks (one scale per row and K-group: activations
+// in the forward GEMM), bit 1 -- B has them (activations in the weight-gradient
+// GEMM).  Such an operand's per-row scale words follow the 2D words in each
+// stage (1 KB per operand, one load per wave) and every lane reads its own
+// row's word instead of the block row's.
+template <bool BF16OUT, bool ACC, int GMODE, int SM>
 __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmArgs g, int tiles_m, int tiles_n,
                                                                           const GroupedArgs gr)
 {
     using F = Fmt<kFmtFp4Block2D>;
     constexpr int RB = F::kRowBytes;                // 64
-    constexpr int kDma = kDmaPerTile;               // 9
+    constexpr bool A1 = (SM & 1) != 0, B1 = (SM & 2) != 0;
+    constexpr int kDma = kDmaPerTile + A1 + B1;     // 9 .. 11
+    constexpr int kWordsA1 = 2 * kCodeBytes + 1024;             // per-row A scale words
+    constexpr int kWordsB1 = kWordsA1 + (A1 ? 1024 : 0);       // per-row B scale words
+    constexpr int kStageBytes = kWordsB1 + (B1 ? 1024 : 0);
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];
     __shared__ int32_t pad_start[GMODE == 0 ? 1 : kMaxSegs + 1];
     __shared__ int32_t tile_start[GMODE == 1 ? kMaxSegs + 1 : 1];
@@ -533,8 +542,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     TileRef lt = ts.ref(cu);
     TileRef ct = lt;
     uint32_t offA[4], offB[4];
-    const uint8_t *lsrc;
+    const uint8_t *lsrc, *lsrcA1 = nullptr, *lsrcB1 = nullptr;
     auto enter = [&]() __attribute__((always_inline)) {
+        if (A1) {
+            int r = lt.m0 + 64 * wave + lane; r = r < lt.M ? r : lt.M - 1;
+            lsrcA1 = lt.sa + (uint32_t)r * (uint32_t)g.ldsa;
+        }
+        if (B1) {
+            int r = lt.n0 + 64 * wave + lane; r = r < lt.N ? r : lt.N - 1;
+            lsrcB1 = lt.sb + (uint32_t)r * (uint32_t)g.ldsb;
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             int ra = lt.m0 + row[j]; ra = ra < lt.M ? ra : lt.M - 1;
@@ -554,16 +571,39 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
         if (v < total) { lu = v; lt = ts.ref(v); lk = 0; enter(); }
         else lk = lt.nk - 1;
     };
-    // load k (0..8) of the cursor's K-tile into ring stage `slot`:
-    //   k = 0..3 A rows 16 (4k + wave) + ..., 4..7 B likewise, 8 the scale words
+    // load k (0 .. kDma-1) of the cursor's K-tile into ring stage `slot`:
+    //   k = 0..3 A rows 16 (4k + wave) + ..., 4..7 B likewise, 8 the 2D scale
+    //   words, then the per-row words of a 1D A (rows 64 wave + lane) and B
     auto load = [&](uint32_t slot, int k) __attribute__((always_inline)) {
         const uint32_t stage = lds0 + (slot % kStages) * kStageBytes;
         if (k < 4)
             lds_dma16(lt.a + lk * RB, offA[k], stage + (4 * k + wave) * 1024);
         else if (k < 8)
             lds_dma16(lt.b + lk * RB, offB[k - 4], stage + kCodeBytes + (4 * (k - 4) + wave) * 1024);
-        else
+        else if (k == 8)
             lds_dma4(lsrc + lk * 4, stage + 2 * kCodeBytes + wave * 256);
+        else if (k == 9 && A1)
+            lds_dma4(lsrcA1 + lk * 4, stage + kWordsA1 + wave * 256);
+        else
+            lds_dma4(lsrcB1 + lk * 4, stage + kWordsB1 + wave * 256);
+    };
+    // scale words of the K-tile in stage `st`: the 2D block-row words (the
+    // same for every lane) or a 1D operand's own row words
+    auto read_scales = [&](const uint8_t *st, uint32_t (&dA)[4], uint32_t (&dB)[4]) __attribute__((always_inline)) {
+        const uint4 wA = *reinterpret_cast<const uint4 *>(st + 2 * kCodeBytes + wave * 256);
+        const uint4 wB = *reinterpret_cast<const uint4 *>(st + 2 * kCodeBytes + wave * 256 + 16);
+        dA[0] = wA.x; dA[1] = wA.y; dA[2] = wA.z; dA[3] = wA.w;
+        dB[0] = wB.x; dB[1] = wB.y; dB[2] = wB.z; dB[3] = wB.w;
+        if (A1) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                dA[i] = *reinterpret_cast<const uint32_t *>(st + kWordsA1 + (wm * 128 + i * 32 + (lane & 31)) * 4);
+        }
+        if (B1) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                dB[j] = *reinterpret_cast<const uint32_t *>(st + kWordsB1 + (wn * 128 + j * 32 + (lane & 31)) * 4);
+        }
     };
 
     const int sw = F::swz(lane & 31);
@@ -595,14 +635,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     }
     wait_vmcnt<(kStages - 1) * kDma>();
     block_barrier();
-    {
-        const uint4 wA = *reinterpret_cast<const uint4 *>(smem + 2 * kCodeBytes + wave * 256);
-        const uint4 wB = *reinterpret_cast<const uint4 *>(smem + 2 * kCodeBytes + wave * 256 + 16);
-        scA[0] = wA.x; scA[1] = wA.y; scA[2] = wA.z; scA[3] = wA.w;
-        scB[0] = wB.x; scB[1] = wB.y; scB[2] = wB.z; scB[3] = wB.w;
+    read_scales(smem, scA, scB);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) Q2D_READ(fa0, fb0, smem, 0, i);
-    }
+    for (int i = 0; i < 4; ++i) Q2D_READ(fa0, fb0, smem, 0, i);
 
     uint32_t s = 0;                                 // ring step
     for (;;) {
@@ -636,17 +671,15 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
             for (int j = 0; j < 4; ++j) {
                 Q2D_MFMA(fa1, fb1, scA, scB, 1, i, j);
                 __builtin_amdgcn_sched_barrier(0);
-                // loads at q = 0, 2, 4, 6, 8, 10..13; fragment reads at q = 1, 3,
-                // 5, 7 (past the last step they are unused); scale words at q = 9
+                // loads at q = 0, 2, 4, 6, 8, 10, 11, ...; fragment reads at
+                // q = 1, 3, 5, 7 (past the last step they are unused); scale
+                // words at q = 9
                 const int q = 4 * i + j;           // 0..15
                 if (q < 8 && (q & 1)) {
                     Q2D_READ(fa0, fb0, sn, 0, q >> 1);
                 } else if (q == 9) {
-                    const uint4 wA = *reinterpret_cast<const uint4 *>(sn + 2 * kCodeBytes + wave * 256);
-                    const uint4 wB = *reinterpret_cast<const uint4 *>(sn + 2 * kCodeBytes + wave * 256 + 16);
-                    nA[0] = wA.x; nA[1] = wA.y; nA[2] = wA.z; nA[3] = wA.w;
-                    nB[0] = wB.x; nB[1] = wB.y; nB[2] = wB.z; nB[3] = wB.w;
-                } else if (q < 14) {
+                    read_scales(sn, nA, nB);
+                } else if (q < kDma + 5) {
                     load(s + kStages, q < 9 ? q >> 1 : q - 5);
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -841,17 +874,33 @@ int cu_count()
 // persistent kernel over at most `tiles` tiles: one workgroup per CU, a
 // multiple of 8 (the XCD count) so that every workgroup stays on one XCD's
 // share of the tile order
-template <bool BF, int GMODE>
+template <bool BF, int GMODE, int SM = 0>
 hipError_t launch_persistent(const GemmArgs &g, const GroupedArgs &gr, int tm, int tn, int64_t tiles, hipStream_t s)
 {
     int64_t grid = cu_count();
     grid = grid < tiles ? grid : tiles;
     grid = (grid + kXcds - 1) / kXcds * kXcds;
     if (g.accumulate)
-        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<BF, true, GMODE>), dim3((unsigned)grid), dim3(kThreads), 0, s, g, tm, tn, gr);
+        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<BF, true, GMODE, SM>), dim3((unsigned)grid), dim3(kThreads), 0, s,
+                           g, tm, tn, gr);
     else
-        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<BF, false, GMODE>), dim3((unsigned)grid), dim3(kThreads), 0, s, g, tm, tn, gr);
+        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<BF, false, GMODE, SM>), dim3((unsigned)grid), dim3(kThreads), 0,
+                           s, g, tm, tn, gr);
     return hipGetLastError();
+}
+
+// dense: the scale mode of the two operands
+template <bool BF>
+hipError_t launch_dense(const GemmArgs &g, int tm, int tn, hipStream_t s)
+{
+    const GroupedArgs none = {nullptr, 0, 0, 0, 0, 0};
+    const int64_t tiles = (int64_t)tm * tn;
+    switch ((g.a1d ? 1 : 0) | (g.b1d ? 2 : 0)) {
+    case 0: return launch_persistent<BF, 0, 0>(g, none, tm, tn, tiles, s);
+    case 1: return launch_persistent<BF, 0, 1>(g, none, tm, tn, tiles, s);
+    case 2: return launch_persistent<BF, 0, 2>(g, none, tm, tn, tiles, s);
+    default: return launch_persistent<BF, 0, 3>(g, none, tm, tn, tiles, s);
+    }
 }
 
 template <int FMT, bool BF>
@@ -871,9 +920,7 @@ hipError_t launch_gemm(const GemmArgs &g, int fmt, int c_is_bf16, hipStream_t st
     const bool off32 = g.M * g.lda <= (int64_t(1) << 32) && g.N * g.ldb <= (int64_t(1) << 32);
     if (fmt == kFmtFp4Block2D && off32 && ((g.M + BM2 - 1) / BM2) * ((g.N + BN2 - 1) / BN2) >= 128) {
         const int tm = (int)((g.M + BM2 - 1) / BM2), tn = (int)((g.N + BN2 - 1) / BN2);
-        const GroupedArgs none = {nullptr, 0, 0, 0, 0, 0};
-        return c_is_bf16 ? launch_persistent<true, 0>(g, none, tm, tn, (int64_t)tm * tn, stream)
-                         : launch_persistent<false, 0>(g, none, tm, tn, (int64_t)tm * tn, stream);
+        return c_is_bf16 ? launch_dense<true>(g, tm, tn, stream) : launch_dense<false>(g, tm, tn, stream);
     }
     if (fmt == kFmtFp4Block2D)
         return c_is_bf16 ? launch_t<kFmtFp4Block2D, true>(g, stream) : launch_t<kFmtFp4Block2D, false>(g, stream);

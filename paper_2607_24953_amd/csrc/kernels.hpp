@@ -30,7 +30,8 @@ struct QuantArgs {
     int64_t store_rows;            // rows of codes / scales written (>= rows; padded rows get zeros)
 };
 
-hipError_t launch_fp4_quantize(const QuantArgs &a, int dtype_bytes, bool stochastic,
+// 2D blocks, or 1D blocks (oned: 1 x 32 rowwise copy, 32 x 1 colwise copy)
+hipError_t launch_fp4_quantize(const QuantArgs &a, int dtype_bytes, bool stochastic, bool oned,
                                hipStream_t stream);
 hipError_t launch_mxfp8_quantize(const QuantArgs &a, int dtype_bytes, hipStream_t stream);
 
@@ -43,6 +44,7 @@ struct GemmArgs {
     void *c;           int64_t ldc;     // elements
     int64_t M, N, K;                    // K rounded up to 128
     int accumulate;
+    int a1d, b1d;                       // FP4: operand with one scale per row and K-group (1x32 blocks)
 };
 
 enum GemmFmt { kFmtFp4Block2D = 0, kFmtMxfp8 = 1 };

@@ -33,6 +33,14 @@
 // own draw; the other nibble of that result is dropped.  The parity tests
 // compare every bfloat16 value under every scale, in both modes, bit for bit
 // with the CPU definition.
+//
+// The same kernel emits 1D FP4 for activations (ONED; Sec. 3, "Application to
+// linear layers"; App. C, "Activations"): 1 x 32 row blocks for the codes copy
+// and 32 x 1 column blocks for the codes_t copy, each with its own
+// truncation-free scale.  A row block spans the 4 lanes that differ in lane
+// bits 0-1, a column block the 4 lanes that differ in bits 4-5; the codes are
+// packed and stored exactly as for 2D blocks, and the scale grids (one byte
+// per row and K-group) go through LDS as 4-byte words.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -104,10 +112,11 @@ __device__ __forceinline__ void philox_block(uint64_t g, uint32_t o0, uint32_t o
 // SR: stochastic rounding.  ALIGNED8: every sub-block row starts at a storage
 // index that is a multiple of 8, so one Philox block serves its 8 elements.
 // GROUPED: the rows are expert segments (see QuantArgs).  WC: 128-column
-// strips per tile (waves side by side).
-template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED, int WC>
+// strips per tile (waves side by side).  ONED: 1 x 32 / 32 x 1 blocks.
+template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED, int WC, bool ONED>
 __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
 {
+    static_assert(!(ONED && GROUPED), "grouped tensors use 2D blocks");
     constexpr int kTC = 128 * WC;
     constexpr int kThreads = 256 * WC;
     constexpr bool PK = sizeof(T) == 2;     // bf16: two elements per register
@@ -205,27 +214,70 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
         return v[i][j];
     };
 
-    // ---- block maximum on |bits| (NaN > inf > finite, as unsigned integers)
+    // ---- block maximum on |bits| (NaN > inf > finite, as unsigned integers).
+    // 2D: one per lane group of 16; 1D: one per row (rm) and per column (cm).
     uint32_t am = 0;
+    uint32_t rm[8], cm[8];
+    if (!ONED) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int k = 0; k < NV; ++k) {
-            if (PK) {
-                const uint32_t w = v[i][k] & 0x7FFF7FFFu;
-                am = max(am, max(w & 0xFFFFu, w >> 16));
-            } else {
-                am = max(am, v[i][k] & 0x7FFFFFFFu);
+            for (int k = 0; k < NV; ++k) {
+                if (PK) {
+                    const uint32_t w = v[i][k] & 0x7FFF7FFFu;
+                    am = max(am, max(w & 0xFFFFu, w >> 16));
+                } else {
+                    am = max(am, v[i][k] & 0x7FFFFFFFu);
+                }
             }
+        if (PK) am <<= 16;
+        am = max(am, (uint32_t)__shfl_xor((int)am, 1));
+        am = max(am, (uint32_t)__shfl_xor((int)am, 2));
+        am = max(am, (uint32_t)__shfl_xor((int)am, 16));
+        am = max(am, (uint32_t)__shfl_xor((int)am, 32));
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) cm[j] = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            uint32_t m = 0;
+#pragma unroll
+            for (int k = 0; k < NV; ++k) {
+                if (PK) {
+                    const uint32_t w = v[i][k] & 0x7FFF7FFFu;
+                    m = max(m, max(w & 0xFFFFu, w >> 16));
+                    cm[2 * k] = max(cm[2 * k], w & 0xFFFFu);
+                    cm[2 * k + 1] = max(cm[2 * k + 1], w >> 16);
+                } else {
+                    const uint32_t w = v[i][k] & 0x7FFFFFFFu;
+                    m = max(m, w);
+                    cm[k] = max(cm[k], w);
+                }
+            }
+            rm[i] = PK ? m << 16 : m;
         }
-    if (PK) am <<= 16;
-    am = max(am, (uint32_t)__shfl_xor((int)am, 1));
-    am = max(am, (uint32_t)__shfl_xor((int)am, 2));
-    am = max(am, (uint32_t)__shfl_xor((int)am, 16));
-    am = max(am, (uint32_t)__shfl_xor((int)am, 32));
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            rm[i] = max(rm[i], (uint32_t)__shfl_xor((int)rm[i], 1));
+            rm[i] = max(rm[i], (uint32_t)__shfl_xor((int)rm[i], 2));
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (PK) cm[j] <<= 16;
+            cm[j] = max(cm[j], (uint32_t)__shfl_xor((int)cm[j], 16));
+            cm[j] = max(cm[j], (uint32_t)__shfl_xor((int)cm[j], 32));
+        }
+    }
     const bool finite = am < 0x7F800000u;
     const int e = fp4_block_exponent(am);
     const float scale = bits_f((uint32_t)(127 + e) << 23);       // 2^e
+    // scale of row i / column j of the sub-block (the block scale for 2D)
+    auto rscale = [&](int i) -> float {
+        return ONED ? bits_f((uint32_t)(127 + fp4_block_exponent(rm[i])) << 23) : scale;
+    };
+    auto cscale = [&](int j) -> float {
+        return ONED ? bits_f((uint32_t)(127 + fp4_block_exponent(cm[j])) << 23) : scale;
+    };
 
     // ---- encode: rowp[i] = eight nibbles of row i, colp[j] = eight nibbles of column j
     uint32_t rowp[8], colp[8];
@@ -233,22 +285,24 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             uint32_t w = 0;
+            const float sc = rscale(i);
             if (PK) {
-                w = rtn_pair_bf16<0>(w, v[i][0], scale);
-                w = rtn_pair_bf16<1>(w, v[i][1], scale);
-                w = rtn_pair_bf16<2>(w, v[i][2], scale);
-                w = rtn_pair_bf16<3>(w, v[i][3], scale);
+                w = rtn_pair_bf16<0>(w, v[i][0], sc);
+                w = rtn_pair_bf16<1>(w, v[i][1], sc);
+                w = rtn_pair_bf16<2>(w, v[i][2], sc);
+                w = rtn_pair_bf16<3>(w, v[i][3], sc);
             } else {
-                w = rtn_pair_f32<0>(w, elem(i, 0), elem(i, 1), scale);
-                w = rtn_pair_f32<1>(w, elem(i, 2), elem(i, 3), scale);
-                w = rtn_pair_f32<2>(w, elem(i, 4), elem(i, 5), scale);
-                w = rtn_pair_f32<3>(w, elem(i, 6), elem(i, 7), scale);
+                w = rtn_pair_f32<0>(w, elem(i, 0), elem(i, 1), sc);
+                w = rtn_pair_f32<1>(w, elem(i, 2), elem(i, 3), sc);
+                w = rtn_pair_f32<2>(w, elem(i, 4), elem(i, 5), sc);
+                w = rtn_pair_f32<3>(w, elem(i, 6), elem(i, 7), sc);
             }
             rowp[i] = w;
         }
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             uint32_t w = 0;
+            const float sc = cscale(j);
             if (PK) {
                 // rows (2m, 2m+1) of column j as one packed pair
                 const int k = j >> 1;
@@ -256,15 +310,15 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
                     const uint32_t lo = v[2 * m][k], hi = v[2 * m + 1][k];
                     return (j & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
                 };
-                w = rtn_pair_bf16<0>(w, pr(0), scale);
-                w = rtn_pair_bf16<1>(w, pr(1), scale);
-                w = rtn_pair_bf16<2>(w, pr(2), scale);
-                w = rtn_pair_bf16<3>(w, pr(3), scale);
+                w = rtn_pair_bf16<0>(w, pr(0), sc);
+                w = rtn_pair_bf16<1>(w, pr(1), sc);
+                w = rtn_pair_bf16<2>(w, pr(2), sc);
+                w = rtn_pair_bf16<3>(w, pr(3), sc);
             } else {
-                w = rtn_pair_f32<0>(w, elem(0, j), elem(1, j), scale);
-                w = rtn_pair_f32<1>(w, elem(2, j), elem(3, j), scale);
-                w = rtn_pair_f32<2>(w, elem(4, j), elem(5, j), scale);
-                w = rtn_pair_f32<3>(w, elem(6, j), elem(7, j), scale);
+                w = rtn_pair_f32<0>(w, elem(0, j), elem(1, j), sc);
+                w = rtn_pair_f32<1>(w, elem(2, j), elem(3, j), sc);
+                w = rtn_pair_f32<2>(w, elem(4, j), elem(5, j), sc);
+                w = rtn_pair_f32<3>(w, elem(6, j), elem(7, j), sc);
             }
             colp[j] = w;
         }
@@ -313,12 +367,13 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int i = 2 * m + h;
+                const float sc = rscale(i);
                 uint32_t acc = 0;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     const f2v pr = {bits_f(elem(i, 2 * k)), bits_f(elem(i, 2 * k + 1))};
-                    const uint32_t lo = sr_pair(k, pr, s16[h][2 * k], scale);
-                    const uint32_t hi = sr_pair(k, pr, s16[h][2 * k + 1] >> 1, scale);
+                    const uint32_t lo = sr_pair(k, pr, s16[h][2 * k], sc);
+                    const uint32_t hi = sr_pair(k, pr, s16[h][2 * k + 1] >> 1, sc);
                     acc |= (lo & (0x0Fu << (8 * k))) | (hi & (0xF0u << (8 * k)));
                 }
                 rowp[i] = acc;
@@ -327,27 +382,50 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const f2v pr = {bits_f(elem(2 * m, j)), bits_f(elem(2 * m + 1, j))};
-                const uint32_t lo = sr_pair(m, pr, s16[0][j], scale);
-                const uint32_t hi = sr_pair(m, pr, s16[1][j] >> 1, scale);
+                const float sc = cscale(j);
+                const uint32_t lo = sr_pair(m, pr, s16[0][j], sc);
+                const uint32_t hi = sr_pair(m, pr, s16[1][j] >> 1, sc);
                 colp[j] |= (lo & (0x0Fu << (8 * m))) | (hi & (0xF0u << (8 * m)));
             }
         }
     }
-    if (!finite) {
+    if (!ONED && !finite) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) { rowp[i] = 0; colp[i] = 0; }
+    }
+    if (ONED) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            if (rm[i] >= 0x7F800000u) rowp[i] = 0;
+            if (cm[i] >= 0x7F800000u) colp[i] = 0;
+        }
     }
 
     // ---- stores through LDS: 16 bytes per lane, codes rows r < store_rows as
     // WC * 64-byte runs, codes_t rows c < C as 64-byte runs
     __shared__ uint32_t st_r[kTile][16 * WC + 1];
     __shared__ uint32_t st_c[kTC][17];
+    __shared__ uint8_t st_rs[ONED ? kTile : 1][4 * WC];     // 1D: row scales of the tile
+    __shared__ uint8_t st_cs[ONED ? kTC : 1][4];            // 1D: column scales of the tile
     {
         const int rl = wr * 32 + 8 * rg;
 #pragma unroll
         for (int i = 0; i < 8; ++i) st_r[rl + i][wc * 16 + cc] = rowp[i];
 #pragma unroll
         for (int j = 0; j < 8; ++j) st_c[wc * 128 + 8 * cc + j][wr * 4 + rg] = colp[j];
+        if (ONED) {
+            auto sbyte = [](uint32_t m) -> uint8_t {
+                return m < 0x7F800000u ? (uint8_t)(127 + fp4_block_exponent(m)) : (uint8_t)0xFF;
+            };
+            if ((cc & 3) == 0) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) st_rs[rl + i][wc * 4 + (cc >> 2)] = sbyte(rm[i]);
+            }
+            if (rg == 0) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) st_cs[wc * 128 + 8 * cc + j][wr] = sbyte(cm[j]);
+            }
+        }
     }
     __syncthreads();
 #pragma unroll
@@ -372,6 +450,28 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
             }
         }
     }
+    if (ONED) {
+        // row r's 4-byte scale word of each 128-column strip; column c's word of
+        // the tile's four row blocks
+        const int t = threadIdx.x;
+        if (t < kTile) {
+            const int64_t r = tr * kTile + t;
+            if (a.scales && r < a.rows) {
+#pragma unroll
+                for (int w = 0; w < WC; ++w)
+                    if (tc * kTC + w * 128 < a.cols_pad)
+                        *reinterpret_cast<uint32_t *>(a.scales + r * a.ld_scales + (tc * kTC + w * 128) / 32) =
+                            *reinterpret_cast<const uint32_t *>(&st_rs[t][4 * w]);
+            }
+        } else if (t >= kThreads - kTC) {
+            const int cl = t - (kThreads - kTC);
+            const int64_t c = tc * kTC + cl;
+            if (a.scales_t && c < a.cols)
+                *reinterpret_cast<uint32_t *>(a.scales_t + c * a.ld_scales_t + tr * 4) =
+                    *reinterpret_cast<const uint32_t *>(&st_cs[cl][0]);
+        }
+        return;
+    }
     if (col_ok && rg == 0 && (cc & 3) == 0) {
         const uint8_t sbyte = finite ? (uint8_t)(e + 127) : (uint8_t)0xFF;
         const int64_t rb = strip_r >> 5, cb = c0 >> 5;
@@ -380,7 +480,7 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
     }
 }
 
-template <typename T, bool VEC, bool SR, bool A8, bool G>
+template <typename T, bool VEC, bool SR, bool A8, bool G, bool ONED>
 hipError_t launch_t(const QuantArgs &a, hipStream_t s)
 {
     // round to nearest is bound by memory traffic: 256-column tiles write whole
@@ -388,33 +488,39 @@ hipError_t launch_t(const QuantArgs &a, hipStream_t s)
     // and keeps 4-wave workgroups for occupancy.
     constexpr int WC = SR ? 1 : 2;
     const int64_t nb = (a.rows_pad / kTile) * ((a.cols_pad + 128 * WC - 1) / (128 * WC));
-    hipLaunchKernelGGL((fp4_quantize_kernel<T, VEC, SR, A8, G, WC>), dim3((unsigned)nb), dim3(256 * WC), 0, s, a);
+    hipLaunchKernelGGL((fp4_quantize_kernel<T, VEC, SR, A8, G, WC, ONED>), dim3((unsigned)nb), dim3(256 * WC), 0, s,
+                       a);
     return hipGetLastError();
 }
 
-template <typename T, bool G>
+template <typename T, bool G, bool ONED>
 hipError_t launch_dtype(const QuantArgs &a, bool vec, bool sr, bool a8, hipStream_t s)
 {
     if (vec) {
-        if (!sr) return launch_t<T, true, false, true, G>(a, s);
-        return a8 ? launch_t<T, true, true, true, G>(a, s) : launch_t<T, true, true, false, G>(a, s);
+        if (!sr) return launch_t<T, true, false, true, G, ONED>(a, s);
+        return a8 ? launch_t<T, true, true, true, G, ONED>(a, s) : launch_t<T, true, true, false, G, ONED>(a, s);
     }
-    return sr ? launch_t<T, false, true, true, G>(a, s) : launch_t<T, false, false, true, G>(a, s);
+    return sr ? launch_t<T, false, true, true, G, ONED>(a, s) : launch_t<T, false, false, true, G, ONED>(a, s);
 }
 
 }  // namespace
 
-hipError_t launch_fp4_quantize(const QuantArgs &a, int dtype_bytes, bool sr, hipStream_t stream)
+hipError_t launch_fp4_quantize(const QuantArgs &a, int dtype_bytes, bool sr, bool oned, hipStream_t stream)
 {
     const uintptr_t base = reinterpret_cast<uintptr_t>(a.x);
     const bool vec = a.stride_c == 1 && (base % 16) == 0 && ((a.stride_r * dtype_bytes) % 16) == 0;
     const bool a8 = (a.stride_r % 8) == 0 && (a.index_base % 8) == 0;
     const bool grouped = a.seg_offsets != nullptr;
+    if (oned) {
+        if (grouped) return hipErrorInvalidValue;
+        return dtype_bytes == 4 ? launch_dtype<float, false, true>(a, vec, sr, a8, stream)
+                                : launch_dtype<uint16_t, false, true>(a, vec, sr, a8, stream);
+    }
     if (dtype_bytes == 4)
-        return grouped ? launch_dtype<float, true>(a, vec, sr, a8, stream)
-                       : launch_dtype<float, false>(a, vec, sr, a8, stream);
-    return grouped ? launch_dtype<uint16_t, true>(a, vec, sr, a8, stream)
-                   : launch_dtype<uint16_t, false>(a, vec, sr, a8, stream);
+        return grouped ? launch_dtype<float, true, false>(a, vec, sr, a8, stream)
+                       : launch_dtype<float, false, false>(a, vec, sr, a8, stream);
+    return grouped ? launch_dtype<uint16_t, true, false>(a, vec, sr, a8, stream)
+                   : launch_dtype<uint16_t, false, false>(a, vec, sr, a8, stream);
 }
 
 }  // namespace q2d

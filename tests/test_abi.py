@@ -39,7 +39,8 @@ def test_exports_every_declared_symbol(q2d):
 @pytest.mark.parametrize("R,C", [(1, 1), (32, 32), (100, 70), (4096, 11008), (131, 257)])
 def test_layout_matches_oracle(q2d, R, C):
     import oracle
-    for fmt, lay in ((q2d.FP4_2D, oracle.fp4_layout(R, C)), (q2d.MXFP8, oracle.mxfp8_layout(R, C))):
+    for fmt, lay in ((q2d.FP4_2D, oracle.fp4_layout(R, C)), (q2d.MXFP8, oracle.mxfp8_layout(R, C)),
+                     (q2d.FP4_1D, oracle.fp4_1d_layout(R, C))):
         d = q2d._Tensor()
         sizes = (ctypes.c_int64 * 4)()
         assert q2d._lib.q2d_tensor_init(ctypes.byref(d), fmt, R, C, 32, sizes) == 0
@@ -91,6 +92,18 @@ def test_error_paths(q2d):
     assert L.q2d_tensor_init(ctypes.byref(f), 1, 64, 64, 32, sizes) == 0
     f.codes, f.scales, f.codes_t, f.scales_t = fake, fake, fake, fake
     assert L.q2d_gemm(ctypes.byref(d), 0, ctypes.byref(f), 0, fake, 0, 64, 0, None) == 1
+    # 1D FP4: the quantizer takes only FP4_1D descriptors and the 2D one only FP4_2D;
+    # a 1D operand pairs with 2D FP4 in a GEMM but not with MXFP8
+    h = q2d._Tensor()
+    assert L.q2d_tensor_init(ctypes.byref(h), 2, 64, 64, 32, sizes) == 0
+    assert L.q2d_quantize_1d(fake, 1, 64, 64, 64, 1, 32, 0, 0, 0, ctypes.byref(h), None) == 1   # no buffers
+    h.codes, h.scales, h.codes_t, h.scales_t = fake, fake, fake, fake
+    assert L.q2d_quantize_1d(fake, 1, 64, 64, 64, 1, 32, 0, 0, 0, ctypes.byref(d), None) == 1   # 2D descriptor
+    assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 32, 0, 0, 0, ctypes.byref(h), None) == 1      # 1D descriptor
+    assert L.q2d_quantize_1d(fake, 1, 64, 64, 64, 1, 64, 0, 0, 0, ctypes.byref(h), None) == 2
+    assert L.q2d_quantize_1d(fake, 1, 64, 64, 64, 1, 32, 9, 0, 0, ctypes.byref(h), None) == 1
+    assert L.q2d_gemm(ctypes.byref(h), 0, ctypes.byref(f), 0, fake, 0, 64, 0, None) == 1
+    assert L.q2d_gemm(ctypes.byref(f), 0, ctypes.byref(h), 0, fake, 0, 64, 0, None) == 1
     assert q2d.q2d_status_string(2) == "unsupported configuration"
 
 
