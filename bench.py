@@ -6,8 +6,9 @@ quantize each activation X and weight W and each output gradient dY once into
 both packed layouts, then run the three GEMMs of every layer, Y = X W^T (bf16
 out), dX = dY W (bf16 out) and dW = dY^T X (fp32 out), reusing the quantized
 operands transposed.  The 7B-class dense workload is the headline; the MoE
-expert FFN (grouped quantizer and grouped GEMMs) and the mixed MXFP8 / FP4 7B
-block are measured in the same run under ``other_workloads``.
+expert FFN (grouped quantizer and grouped GEMMs), the mixed MXFP8 / FP4 7B
+block and the 7B linears with 1D-block activations (the paper's placement) are
+measured in the same run under ``other_workloads``.
 
 Prints one JSON line.  ``value`` = algorithmic GEMM flops of the step / wall
 time of the whole step (quantizers included) with all inputs resident in HBM.
@@ -45,6 +46,10 @@ WORKLOAD_TEXT = {
                "(Zipf 1.1 routing, 131072 token slots), hidden 2048, expert FFN 768 (gate+up "
                "2048->1536, down 768->2048); grouped 32x32 2D-block FP4 (X, W round-to-nearest; "
                "dY stochastic)",
+    "dense_7b_1d": "7B-class dense linears fwd+bwd (shapes and tensors of dense_7b) with the paper's "
+                   "quantization placement: activations X in 1D FP4 (1x32 blocks for the forward "
+                   "GEMM, 32x1 for the weight gradient), W and dY in 32x32 2D-block FP4 (X, W "
+                   "round-to-nearest; dY stochastic)",
     "mixed_7b": "7B-class block fwd+bwd, tokens 16384: Q/K projections in MXFP8 (E4M3, 1x32) "
                 "and V, O, gate, up, down in 32x32 2D-block FP4 with stochastic rounding; "
                 "bf16 inputs with outlier channels",
@@ -56,10 +61,12 @@ KIND_PEAK = {"gemm_fp4": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
              "gemm_fp8": ("mfma", PEAK_FP8_TFLOPS, "TFLOP/s"),
              "quant_fp4": ("hbm", PEAK_HBM_GBS, "GB/s"),
              "quant_fp4_grouped": ("hbm", PEAK_HBM_GBS, "GB/s"),
+             "quant_fp4_1d": ("hbm", PEAK_HBM_GBS, "GB/s"),
              "quant_mxfp8": ("hbm", PEAK_HBM_GBS, "GB/s")}
 KIND_KERNEL = {"gemm_fp4": "gemm_fp4_persistent_kernel", "gemm_fp4_grouped": "gemm_fp4_persistent_kernel (grouped)",
                "gemm_fp8": "gemm_fp8_256_kernel", "quant_fp4": "fp4_quantize_kernel",
                "quant_fp4_grouped": "fp4_quantize_kernel (grouped)",
+               "quant_fp4_1d": "fp4_quantize_kernel (1D blocks)",
                "quant_mxfp8": "mxfp8_quantize_kernel"}
 
 
@@ -69,7 +76,7 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="dense_7b", choices=sorted(WORKLOAD_TEXT))
-    p.add_argument("--also", default="moe_30b,mixed_7b",
+    p.add_argument("--also", default="moe_30b,mixed_7b,dense_7b_1d",
                    help="further workloads measured in the same run (comma list, or 'none')")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-tokens", type=int, default=256)
@@ -92,25 +99,29 @@ def copy_calibration(torch, nbytes: int, reps: int = 3):
 
 def quant_bytes(t, fmt="fp4") -> float:
     """Algorithmic bytes of one quantization: the input once, both code layouts, scales.
-    FP4: two 4-bit layouts and one E8M0 byte per 32x32 block; MXFP8: two 8-bit layouts
-    and one E8M0 byte per 32 elements in each layout."""
+    FP4: two 4-bit layouts and one E8M0 byte per 32x32 block; 1D FP4: two 4-bit layouts
+    and one E8M0 byte per 32 elements in each; MXFP8: two 8-bit layouts and one E8M0
+    byte per 32 elements in each layout."""
     n = t.numel()
     if fmt == "mxfp8":
         return n * t.element_size() + 2.0 * n + 2.0 * n / 32.0
+    if fmt == "fp4_1d":
+        return n * t.element_size() + n * 0.5 * 2 + 2.0 * n / 32.0
     return n * t.element_size() + n * 0.5 * 2 + n / 1024.0
 
 
-def gemm_bytes(a_elems, b_elems, c_bytes, fmt="fp4") -> float:
+def gemm_bytes(a_elems, b_elems, c_bytes, fmt="fp4", a1d=False, b1d=False) -> float:
     """Algorithmic HBM bytes of one GEMM: both quantized operands once (codes and
-    scales) and the output once."""
+    scales) and the output once (a1d / b1d: that FP4 operand has 1x32 blocks)."""
     if fmt == "mxfp8":
         return (a_elems + b_elems) * (1.0 + 1.0 / 32.0) + c_bytes
-    return (a_elems + b_elems) * (0.5 + 1.0 / 1024.0) + c_bytes
+    return (a_elems * (0.5 + (1.0 / 32.0 if a1d else 1.0 / 1024.0)) +
+            b_elems * (0.5 + (1.0 / 32.0 if b1d else 1.0 / 1024.0)) + c_bytes)
 
 
 KIND_SOURCES = {"gemm_fp4": "gemm.hip", "gemm_fp4_grouped": "gemm.hip", "gemm_fp8": "gemm.hip",
                 "quant_fp4": "quantize_fp4.hip", "quant_fp4_grouped": "quantize_fp4.hip",
-                "quant_mxfp8": "quantize_mxfp8.hip"}
+                "quant_fp4_1d": "quantize_fp4.hip", "quant_mxfp8": "quantize_mxfp8.hip"}
 
 
 def kind_hash(kind: str) -> str:
@@ -130,8 +141,11 @@ def kind_of(kernel_name: str):
         return "gemm_fp4" if m.group(1) == "0" else "gemm_fp8"
     m = re.search(r"fp4_quantize_kernel<([^>]*)>", kernel_name)
     if m:
-        # template arguments: element type, VEC, SR, ALIGNED8, GROUPED, column waves
-        return "quant_fp4_grouped" if m.group(1).split(",")[4].strip() == "true" else "quant_fp4"
+        # template arguments: element type, VEC, SR, ALIGNED8, GROUPED, column waves, 1D
+        a = [t.strip() for t in m.group(1).split(",")]
+        if a[6] == "true":
+            return "quant_fp4_1d"
+        return "quant_fp4_grouped" if a[4] == "true" else "quant_fp4"
     if "mxfp8_quantize_kernel" in kernel_name:
         return "quant_mxfp8"
     return None
@@ -182,13 +196,22 @@ class Step:
     def _dense(self):
         q2d, torch, w, dev = self.q2d, self.torch, self.w, self.dev
         qt = {}
+        fmt_of = lambda lin, name: lin.x_fmt if (name == lin.x and lin.x_fmt) else lin.fmt
         for lin in w.linears:
             for name in (lin.x, lin.w, lin.dy):
-                key = (name, lin.fmt)
+                fmt = fmt_of(lin, name)
+                key = (name, fmt)
                 if key in qt:
                     continue
                 t = w.tensors[name]
-                if lin.fmt == "mxfp8":
+                if fmt == "fp4_1d":
+                    qt[key] = q2d.QTensor(q2d.FP4_1D, t.shape[0], t.shape[1], dev)
+                    off = len(qt)
+                    b = quant_bytes(t, "fp4_1d")
+                    self.ops.append(("quant_fp4_1d", name + ".1d", b, b,
+                                     lambda t=t, o=qt[key], m=w.rounding[name], off=off:
+                                     q2d.q2d_quantize_1d(t, m, w.seed, off, out=o)))
+                elif fmt == "mxfp8":
                     qt[key] = q2d.QTensor(q2d.MXFP8, t.shape[0], t.shape[1], dev)
                     b = quant_bytes(t, "mxfp8")
                     self.ops.append(("quant_mxfp8", name + ".mxfp8", b, b,
@@ -201,18 +224,19 @@ class Step:
                                      lambda t=t, o=qt[key], m=w.rounding[name], off=off:
                                      q2d.q2d_quantize(t, m, w.seed, off, out=o)))
         for lin in w.linears:
-            qx, qw, qdy = qt[(lin.x, lin.fmt)], qt[(lin.w, lin.fmt)], qt[(lin.dy, lin.fmt)]
+            x1d = fmt_of(lin, lin.x) == "fp4_1d"
+            qx, qw, qdy = qt[(lin.x, fmt_of(lin, lin.x))], qt[(lin.w, lin.fmt)], qt[(lin.dy, lin.fmt)]
             Y = torch.empty((lin.tokens, lin.n_out), dtype=torch.bfloat16, device=dev)
             dX = torch.empty((lin.tokens, lin.k_in), dtype=torch.bfloat16, device=dev)
             dW = torch.empty((lin.n_out, lin.k_in), dtype=torch.float32, device=dev)
             f = 2.0 * lin.tokens * lin.n_out * lin.k_in
             kind = "gemm_fp8" if lin.fmt == "mxfp8" else "gemm_fp4"
             T, N, K = lin.tokens, lin.n_out, lin.k_in
-            for nm, a, ta, b, tb, out, mnk in (("fwd", qx, 0, qw, 0, Y, (T, N, K)),
-                                               ("dX", qdy, 0, qw, 1, dX, (T, K, N)),
-                                               ("dW", qdy, 1, qx, 1, dW, (N, K, T))):
+            for nm, a, ta, b, tb, out, mnk, a1, b1 in (("fwd", qx, 0, qw, 0, Y, (T, N, K), x1d, False),
+                                                       ("dX", qdy, 0, qw, 1, dX, (T, K, N), False, False),
+                                                       ("dW", qdy, 1, qx, 1, dW, (N, K, T), False, x1d)):
                 M_, N_, K_ = mnk
-                ab = gemm_bytes(M_ * K_, N_ * K_, out.numel() * out.element_size(), lin.fmt)
+                ab = gemm_bytes(M_ * K_, N_ * K_, out.numel() * out.element_size(), lin.fmt, a1, b1)
                 self.ops.append((kind, "%s.%s" % (lin.name, nm), f, ab,
                                  lambda a=a, ta=ta, b=b, tb=tb, out=out:
                                  q2d.q2d_gemm(a, ta, b, tb, out=out)))
@@ -340,18 +364,19 @@ def cpu_baseline(w, tokens: int):
                       "%.3f TFLOP" % (len(w.linears), tokens, dt, flops / 1e12)}
 
 
-PROFILE_WORKLOADS = ("dense_7b", "moe_30b", "mixed_7b")
+PROFILE_WORKLOADS = ("dense_7b", "moe_30b", "mixed_7b", "dense_7b_1d")
 PROFILE_FILES = {
     "dense_7b": [("gemm_fp4_persistent_kernel.dense_7b.md", ("gemm_fp4",)),
                  ("fp4_quantize_kernel.dense_7b.md", ("quant_fp4",))],
     "moe_30b": [("grouped_fp4_kernels.moe_30b.md", ("gemm_fp4_grouped", "quant_fp4_grouped", "quant_fp4"))],
+    "dense_7b_1d": [("fp4_1d_kernels.dense_7b_1d.md", ("quant_fp4_1d", "gemm_fp4", "quant_fp4"))],
     "mixed_7b": [("mxfp8_kernels.mixed_7b.md", ("gemm_fp8", "quant_mxfp8", "gemm_fp4", "quant_fp4"))],
 }
 PROFILE_COMMANDS = """cd /tmp && export TMPDIR=/tmp; R=/root/repo; O=$R/gpurun_out/pb
 rocprofv3 --kernel-trace --stats --output-format csv -d $O/trace -o bench -- python3 $R/bench.py > $O/bench_trace.log 2>&1
 for c in FETCH_SIZE WRITE_SIZE; do
   rocprofv3 --pmc $c --output-format csv -d $O/copy_$c -o copy -- python3 $R/bench.py --copy-calibration 1073741824 > $O/copy_$c.log 2>&1
-  for wl in dense_7b moe_30b mixed_7b; do
+  for wl in dense_7b moe_30b mixed_7b dense_7b_1d; do
     rocprofv3 --pmc $c --output-format csv -d $O/${wl}_$c -o $wl -- python3 $R/bench.py --workload $wl --also none --steps 1 --warmup 0 --no-cpu-baseline > $O/${wl}_$c.log 2>&1
   done
 done

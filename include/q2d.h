@@ -92,10 +92,15 @@ typedef enum {
  * FP4_1D (activations; Sec. 3, "Application to linear layers"; App. C,
  * "Activations"):
  *   codes / codes_t packed exactly as for FP4_2D;
- *   scales   [rows][ld_scales]: byte (r, c/32) is the scale of the 1x32 block
- *            of row r (K = cols);
- *   scales_t [cols][ld_scales_t]: byte (c, r/32) is the scale of the 32x1
- *            block of column c (K = rows).
+ *   scales   [roundup(cols,128)/128][ld_scales >= 4*rows]: one 4-byte word per
+ *            row and K-tile of 128 columns; the scale of the 1x32 block J of
+ *            row r (K = cols) is byte J % 4 of word (J / 4, r), i.e.
+ *            scales[(J / 4) * ld_scales + 4 r + J % 4];
+ *   scales_t [roundup(rows,128)/128][ld_scales_t >= 4*cols]: likewise for the
+ *            32x1 block I of column c (K = rows): scales_t[(I / 4) * ld_scales_t
+ *            + 4 c + I % 4].
+ *   (K-tile-major words put the scales a GEMM K-tile needs for consecutive
+ *   rows at consecutive addresses.)
  *   The two copies have different blocks, scales and (in general) codes: the
  *   forward/backward inconsistency of 1D layouts (Sec. 2) that the 2D blocks
  *   of weights and gradients avoid.

@@ -160,14 +160,21 @@ def mxfp8_layout(R: int, C: int) -> dict:
 
 
 def fp4_1d_layout(R: int, C: int) -> dict:
-    """1D FP4: codes packed as for 2D blocks, one scale per row (per column for
-    the transposed copy) and 32-element K-group."""
+    """1D FP4: codes packed as for 2D blocks; one scale per row (per column for
+    the transposed copy) and 32-element K-group, stored as one 4-byte word per
+    row and K-tile of 128: [K-tiles][rows * 4] bytes."""
     return {
         "codes": (R, _rup(C, 128) // 2),
-        "scales": (R, _rup(C, 128) // 32),
+        "scales": (_rup(C, 128) // 128, 4 * R),
         "codes_t": (C, _rup(R, 128) // 2),
-        "scales_t": (C, _rup(R, 128) // 32),
+        "scales_t": (_rup(R, 128) // 128, 4 * C),
     }
+
+
+def scale_grid_1d(words: np.ndarray, rows: int) -> np.ndarray:
+    """The [rows][K-groups] E8M0 bytes of a 1D scale buffer in word layout."""
+    nkt = words.shape[0]
+    return words.reshape(nkt, -1, 4)[:, :rows].transpose(1, 0, 2).reshape(rows, nkt * 4)
 
 
 def grouped_rows(offsets) -> np.ndarray:
@@ -350,7 +357,7 @@ def dequant_fp4(codes: np.ndarray, scales: np.ndarray, R: int, C: int) -> np.nda
 def dequant_fp4_1d(codes: np.ndarray, scales: np.ndarray, R: int, C: int) -> np.ndarray:
     """R x C float64 values of a 1x32-block FP4 operand (row r, K index c)."""
     q = fp4_values(_unpack(codes[:R], C))
-    s = _scale_values(scales[:R])
+    s = _scale_values(scale_grid_1d(scales, R))
     return q * s[:, np.arange(C) // 32]
 
 

@@ -233,10 +233,14 @@ void or_quantize_fp4_2d(const void *x, int dtype, int64_t R, int64_t C, int64_t 
  * block gets the truncation-free E8M0 scale of the 2D method (Sec. 3.1) and its
  * elements the same E2M1 codec; a stochastic element uses its one storage-index
  * draw in both copies.
- *   rowwise: codes [R][ldc] (byte (r, c/2), low nibble = even c), scales [R][lds]
- *            (entry (r, c/32));
- *   colwise: codes_t [C][ldt] (byte (c, r/2), low nibble = even r),
- *            scales_t [C][ldst] (entry (c, r/32)).
+ *   rowwise: codes [R][ldc] (byte (r, c/2), low nibble = even c); scales as
+ *            4-byte words, one per row and K-tile of 128 columns: the scale of
+ *            block (r, J) is byte J % 4 of word (J / 4, r), at
+ *            scales[(J / 4) * lds + 4 r + J % 4];
+ *   colwise: codes_t [C][ldt] (byte (c, r/2), low nibble = even r); the scale
+ *            of block (I, c) at scales_t[(I / 4) * ldst + 4 c + I % 4].
+ * (The word layout is the library's storage contract: a GEMM K-tile reads the
+ * words of consecutive rows from consecutive addresses.)
  */
 void or_quantize_fp4_1d(const void *x, int dtype, int64_t R, int64_t C, int64_t sr, int64_t sc,
                         int mode, uint64_t seed, uint64_t offset,
@@ -258,7 +262,7 @@ void or_quantize_fp4_1d(const void *x, int dtype, int64_t R, int64_t C, int64_t 
                 if (!isfinite(v)) finite = 0; else if (fabs(v) > M) M = fabs(v);
             }
             int e = or_fp4_scale_exponent(M);
-            scales[r * lds + J] = finite ? (uint8_t)(e + 127) : 0xFF;
+            scales[(J / 4) * lds + 4 * r + J % 4] = finite ? (uint8_t)(e + 127) : 0xFF;
             for (int64_t c = J * 32; c < c1; ++c) {
                 unsigned code = 0;
                 if (finite) {
@@ -283,7 +287,7 @@ void or_quantize_fp4_1d(const void *x, int dtype, int64_t R, int64_t C, int64_t 
                 if (!isfinite(v)) finite = 0; else if (fabs(v) > M) M = fabs(v);
             }
             int e = or_fp4_scale_exponent(M);
-            scales_t[c * ldst + I] = finite ? (uint8_t)(e + 127) : 0xFF;
+            scales_t[(I / 4) * ldst + 4 * c + I % 4] = finite ? (uint8_t)(e + 127) : 0xFF;
             for (int64_t r = I * 32; r < r1; ++r) {
                 unsigned code = 0;
                 if (finite) {

@@ -29,10 +29,11 @@ Layout layout_of(q2d_fmt fmt, int64_t R, int64_t C)
         l.ld_scales = rup(C, kPadK) / 32; l.rows_scales = cdiv(R, 32);
         l.ld_scales_t = rup(R, kPadK) / 32; l.rows_scales_t = cdiv(C, 32);
     } else if (fmt == Q2D_FMT_FP4_1D) {
+        // scales: one 4-byte word per row and K-tile, K-tile major
         l.ld_codes = rup(C, kPadK) / 2;   l.rows_codes = R;
         l.ld_codes_t = rup(R, kPadK) / 2; l.rows_codes_t = C;
-        l.ld_scales = rup(C, kPadK) / 32; l.rows_scales = R;
-        l.ld_scales_t = rup(R, kPadK) / 32; l.rows_scales_t = C;
+        l.ld_scales = 4 * R;              l.rows_scales = rup(C, kPadK) / kPadK;
+        l.ld_scales_t = 4 * C;            l.rows_scales_t = rup(R, kPadK) / kPadK;
     } else {
         l.ld_codes = rup(C, kPadK);       l.rows_codes = R;
         l.ld_codes_t = rup(R, kPadK);     l.rows_codes_t = C;

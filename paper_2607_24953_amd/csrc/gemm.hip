@@ -122,8 +122,9 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmArgs g, int64_
     for (int i = 0; i < 2; ++i) {
         int64_t ra = m0 + wm * 64 + i * 32 + (lane & 31); ra = ra < g.M ? ra : g.M - 1;
         int64_t rb = n0 + wn * 64 + i * 32 + (lane & 31); rb = rb < g.N ? rb : g.N - 1;
-        sa_row[i] = g.sa + (ra >> (g.a1d ? 0 : F::kScaleRowShift)) * g.ldsa;
-        sb_row[i] = g.sb + (rb >> (g.b1d ? 0 : F::kScaleRowShift)) * g.ldsb;
+        // 1x32 FP4 scales are K-tile-major words (row offset 4 r, K-tile stride ld)
+        sa_row[i] = g.a1d ? g.sa + ra * 4 : g.sa + (ra >> F::kScaleRowShift) * g.ldsa;
+        sb_row[i] = g.b1d ? g.sb + rb * 4 : g.sb + (rb >> F::kScaleRowShift) * g.ldsb;
     }
 
     v16f acc[2][2];
@@ -160,8 +161,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmArgs g, int64_
         uint32_t swa[2], swb[2];
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
-            swa[i] = *reinterpret_cast<const uint32_t *>(sa_row[i] + kt * 4);
-            swb[i] = *reinterpret_cast<const uint32_t *>(sb_row[i] + kt * 4);
+            swa[i] = *reinterpret_cast<const uint32_t *>(sa_row[i] + kt * (g.a1d ? g.ldsa : 4));
+            swb[i] = *reinterpret_cast<const uint32_t *>(sb_row[i] + kt * (g.b1d ? g.ldsb : 4));
         }
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
@@ -544,13 +545,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     uint32_t offA[4], offB[4];
     const uint8_t *lsrc, *lsrcA1 = nullptr, *lsrcB1 = nullptr;
     auto enter = [&]() __attribute__((always_inline)) {
+        // 1x32 scales are K-tile-major words: row r of K-tile k at k * ld + 4 r
         if (A1) {
             int r = lt.m0 + 64 * wave + lane; r = r < lt.M ? r : lt.M - 1;
-            lsrcA1 = lt.sa + (uint32_t)r * (uint32_t)g.ldsa;
+            lsrcA1 = lt.sa + 4 * r;
         }
         if (B1) {
             int r = lt.n0 + 64 * wave + lane; r = r < lt.N ? r : lt.N - 1;
-            lsrcB1 = lt.sb + (uint32_t)r * (uint32_t)g.ldsb;
+            lsrcB1 = lt.sb + 4 * r;
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -563,6 +565,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
         const int lim = isA ? lt.M : lt.N;
         int r = (isA ? lt.m0 : lt.n0) + srow; r = r < lim ? r : lim - 1;
         lsrc = (isA ? lt.sa : lt.sb) + (uint32_t)(r >> 5) * (uint32_t)(isA ? g.ldsa : g.ldsb);
+        // a 1D operand has no block-row words: its lanes read the start of its own
+        // word buffer instead (word k of K-tile 0 .. lies inside it for every
+        // K-tile k), and the bytes are never used
+        if ((A1 && isA) || (B1 && !isA)) lsrc = isA ? lt.sa : lt.sb;
     };
     enter();
     auto advance = [&]() __attribute__((always_inline)) {
@@ -583,9 +589,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
         else if (k == 8)
             lds_dma4(lsrc + lk * 4, stage + 2 * kCodeBytes + wave * 256);
         else if (k == 9 && A1)
-            lds_dma4(lsrcA1 + lk * 4, stage + kWordsA1 + wave * 256);
+            lds_dma4(lsrcA1 + lk * (uint32_t)g.ldsa, stage + kWordsA1 + wave * 256);
         else
-            lds_dma4(lsrcB1 + lk * 4, stage + kWordsB1 + wave * 256);
+            lds_dma4(lsrcB1 + lk * (uint32_t)g.ldsb, stage + kWordsB1 + wave * 256);
     };
     // scale words of the K-tile in stage `st`: the 2D block-row words (the
     // same for every lane) or a 1D operand's own row words

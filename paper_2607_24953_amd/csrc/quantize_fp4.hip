@@ -39,8 +39,8 @@
 // and 32 x 1 column blocks for the codes_t copy, each with its own
 // truncation-free scale.  A row block spans the 4 lanes that differ in lane
 // bits 0-1, a column block the 4 lanes that differ in bits 4-5; the codes are
-// packed and stored exactly as for 2D blocks, and the scale grids (one byte
-// per row and K-group) go through LDS as 4-byte words.
+// packed and stored exactly as for 2D blocks, and the scales (one byte per row
+// and K-group) go through LDS and leave as 4-byte words in K-tile-major order.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -451,8 +451,8 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
         }
     }
     if (ONED) {
-        // row r's 4-byte scale word of each 128-column strip; column c's word of
-        // the tile's four row blocks
+        // scale words, K-tile major: row r's word of each 128-column strip k at
+        // (k, r); column c's word of this 128-row tile at (tr, c)
         const int t = threadIdx.x;
         if (t < kTile) {
             const int64_t r = tr * kTile + t;
@@ -460,14 +460,14 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
 #pragma unroll
                 for (int w = 0; w < WC; ++w)
                     if (tc * kTC + w * 128 < a.cols_pad)
-                        *reinterpret_cast<uint32_t *>(a.scales + r * a.ld_scales + (tc * kTC + w * 128) / 32) =
+                        *reinterpret_cast<uint32_t *>(a.scales + ((tc * kTC + w * 128) / 128) * a.ld_scales + 4 * r) =
                             *reinterpret_cast<const uint32_t *>(&st_rs[t][4 * w]);
             }
         } else if (t >= kThreads - kTC) {
             const int cl = t - (kThreads - kTC);
             const int64_t c = tc * kTC + cl;
             if (a.scales_t && c < a.cols)
-                *reinterpret_cast<uint32_t *>(a.scales_t + c * a.ld_scales_t + tr * 4) =
+                *reinterpret_cast<uint32_t *>(a.scales_t + tr * a.ld_scales_t + 4 * c) =
                     *reinterpret_cast<const uint32_t *>(&st_cs[cl][0]);
         }
         return;

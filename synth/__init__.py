@@ -28,7 +28,7 @@ import torch
 
 __all__ = [
     "normal", "add_outlier_channels", "moe_counts", "segment_offsets",
-    "Workload", "tiny", "dense_1b", "dense_7b", "moe_30b", "mixed_7b", "WORKLOADS",
+    "Workload", "tiny", "dense_1b", "dense_7b", "dense_7b_1d", "moe_30b", "mixed_7b", "WORKLOADS",
 ]
 
 
@@ -97,6 +97,7 @@ class Linear:
     n_out: int
     k_in: int
     fmt: str = "fp4"          # "fp4" (2D-block FP4) or "mxfp8"
+    x_fmt: str = ""           # format of X when it differs: "fp4_1d" (1D-block FP4)
 
     @property
     def flops(self) -> int:
@@ -181,6 +182,17 @@ def dense_7b(device="cpu") -> Workload:
     return Workload("dense_7b", t, lin, rnd, seed=3)
 
 
+def dense_7b_1d(device="cpu") -> Workload:
+    """The dense_7b tensors and linears with the paper's activation placement: X in
+    1D-block FP4 (1x32 along K_in for the forward GEMM, 32x1 along tokens for the
+    weight gradient), W and dY in 2D blocks."""
+    w = dense_7b(device)
+    for lin in w.linears:
+        lin.x_fmt = "fp4_1d"
+    w.name = "dense_7b_1d"
+    return w
+
+
 def mixed_7b(device="cpu") -> Workload:
     """7B block with Q/K projections in MXFP8 and V, O, gate, up, down in 2D-block FP4 (SR)."""
     T, H, F = 16384, 4096, 11008
@@ -222,5 +234,5 @@ def moe_30b(device="cpu", tokens: int = 16384, experts: int = 128, topk: int = 8
     return w
 
 
-WORKLOADS = {"tiny": tiny, "dense_1b": dense_1b, "dense_7b": dense_7b,
+WORKLOADS = {"tiny": tiny, "dense_1b": dense_1b, "dense_7b": dense_7b, "dense_7b_1d": dense_7b_1d,
              "moe_30b": moe_30b, "mixed_7b": mixed_7b}

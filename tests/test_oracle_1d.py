@@ -41,7 +41,7 @@ def test_rowwise_reduces_to_2d_on_row_replicated_blocks(shape, mode):
     q1 = oracle.quantize_fp4_1d(x, mode, seed=3, offset=4)
     q2 = oracle.quantize_fp4_2d(x, mode, seed=3, offset=4)
     np.testing.assert_array_equal(q1["codes"], q2["codes"])
-    np.testing.assert_array_equal(q1["scales"], q2["scales"][np.arange(R) // B])
+    np.testing.assert_array_equal(oracle.scale_grid_1d(q1["scales"], R), q2["scales"][np.arange(R) // B])
 
 
 @pytest.mark.parametrize("shape", [(96, 160), (70, 100), (65, 33)])
@@ -53,7 +53,7 @@ def test_colwise_reduces_to_2d_on_column_replicated_blocks(shape, mode):
     q1 = oracle.quantize_fp4_1d(x, mode, seed=8, offset=1)
     q2 = oracle.quantize_fp4_2d(x, mode, seed=8, offset=1)
     np.testing.assert_array_equal(q1["codes_t"], q2["codes_t"])
-    np.testing.assert_array_equal(q1["scales_t"], q2["scales_t"][np.arange(C) // B])
+    np.testing.assert_array_equal(oracle.scale_grid_1d(q1["scales_t"], C), q2["scales_t"][np.arange(C) // B])
 
 
 @pytest.mark.parametrize("mode", ["rtn", "sr"])
@@ -82,12 +82,13 @@ def test_hand_derived_block():
     x = np.zeros((32, 32), dtype=np.float32)
     x[0, :4] = [7.0, 0.75, -2.5, 1.25]
     q = oracle.quantize_fp4_1d(x, "rtn")
-    assert q["scales"][0, 0] == 128
+    sg, sgt = oracle.scale_grid_1d(q["scales"], 32), oracle.scale_grid_1d(q["scales_t"], 32)
+    assert sg[0, 0] == 128 and q["scales"][0, 0] == 128    # byte 0 of word (0, row 0)
     assert list(_unpack(q["codes"], 32)[0, :5]) == [6, 1, 10, 1, 0]
-    assert q["scales"][1, 0] == 0                          # all-zero row block: byte 0x00
-    assert q["scales_t"][0, 0] == 128 and _unpack(q["codes_t"], 32)[0, 0] == 6
+    assert sg[1, 0] == 0                                   # all-zero row block: byte 0x00
+    assert sgt[0, 0] == 128 and _unpack(q["codes_t"], 32)[0, 0] == 6
     # column 1 is 0.75 alone: 6 * 2^-3 < 0.75 <= 6 * 2^-2, e = -3, 0.75 / 2^-3 = 6 (index 7)
-    assert q["scales_t"][1, 0] == 124 and _unpack(q["codes_t"], 32)[1, 0] == 7
+    assert sgt[1, 0] == 124 and q["scales_t"][0, 4] == 124 and _unpack(q["codes_t"], 32)[1, 0] == 7
 
 
 def test_forward_backward_inconsistency_of_1d_blocks():
@@ -117,15 +118,16 @@ def test_elementwise_definition(shape, mode):
     nbc = -(-C // B)
     rmax = np.stack([np.abs(x64[:, j * B:(j + 1) * B]).max(axis=1) for j in range(nbc)], axis=1)
     er = np.vectorize(oracle.fp4_scale_exponent)(rmax).astype(np.int64)
-    np.testing.assert_array_equal(q["scales"][:, :nbc], (er + 127).astype(np.uint8))
-    assert not q["scales"][:, nbc:].any()
+    sg = oracle.scale_grid_1d(q["scales"], R)
+    np.testing.assert_array_equal(sg[:, :nbc], (er + 127).astype(np.uint8))
+    assert not sg[:, nbc:].any()
     want = oracle.fp4_codes(x64, er[:, np.arange(C) // B], mode == "sr", r16)
     np.testing.assert_array_equal(_unpack(q["codes"], C), want)
     # colwise: block maxima along rows
     nbr = -(-R // B)
     cmax = np.stack([np.abs(x64[i * B:(i + 1) * B, :]).max(axis=0) for i in range(nbr)], axis=0)
     ec = np.vectorize(oracle.fp4_scale_exponent)(cmax).astype(np.int64)
-    np.testing.assert_array_equal(q["scales_t"][:, :nbr], (ec.T + 127).astype(np.uint8))
+    np.testing.assert_array_equal(oracle.scale_grid_1d(q["scales_t"], C)[:, :nbr], (ec.T + 127).astype(np.uint8))
     wantc = oracle.fp4_codes(x64, ec[np.arange(R) // B, :], mode == "sr", r16)
     np.testing.assert_array_equal(_unpack(q["codes_t"], R), wantc.T)
     # round to nearest: |Q(x) - x| <= S * delta / 2 <= S (largest E2M1 spacing is 2)
