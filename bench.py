@@ -446,8 +446,9 @@ def summarize_profiles(d: str, out_dir: str):
         f.write("\n")
 
     # kernel trace of the default benchmark run: dispatches split by workload phase
-    # (the workloads run in order; the first grouped launch starts the MoE phase and
-    # the first MXFP8 launch the mixed phase)
+    # (the workloads run in order; the first grouped launch starts the MoE phase, the
+    # first MXFP8 launch the mixed phase and the first 1D quantization the phase of
+    # the 7B linears with 1D activations)
     bt = _json_line(os.path.join(d, "bench_trace.log"))
     events = {bt["config"]["name"]: bt["kinds"]}
     for wl, o in bt.get("other_workloads", {}).items():
@@ -463,6 +464,8 @@ def summarize_profiles(d: str, out_dir: str):
             phase = "moe_30b"
         if kind.endswith("mxfp8") or kind == "gemm_fp8":
             phase = "mixed_7b"
+        if kind == "quant_fp4_1d":
+            phase = "dense_7b_1d"
         a = durs.setdefault((phase, kind), [0.0, 0])
         a[0] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-6; a[1] += 1
     stats = _csv(os.path.join(d, "trace"), "_kernel_stats.csv")
