@@ -280,7 +280,10 @@ __device__ __forceinline__ void wait_vmcnt() { asm volatile("s_waitcnt vmcnt(%0)
 __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 // Write a wave's 128 x 128 accumulator block (4 x 4 MFMA tiles) to C; CHECK
-// masks rows >= M and columns >= N.  bf16 output rounds to nearest even.
+// masks rows >= M and columns >= N.  bf16 output rounds to nearest even.  The
+// stores are non-temporal: every CU writes its tile at about the same time,
+// and C is not read again by the kernel, so it should not displace the operand
+// lines the next tiles reuse from L2.
 template <bool BF16OUT, bool ACC, bool CHECK>
 __device__ __forceinline__ void store_tile(v16f (&acc)[4][4], const GemmArgs &g, int64_t row0, int64_t col0)
 {
@@ -301,11 +304,11 @@ __device__ __forceinline__ void store_tile(v16f (&acc)[4][4], const GemmArgs &g,
                 if (BF16OUT) {
                     __bf16 *p = reinterpret_cast<__bf16 *>(prow + j * 32 * 2);
                     if (ACC) v += (float)*p;
-                    *p = (__bf16)v;
+                    __builtin_nontemporal_store((__bf16)v, p);
                 } else {
                     float *p = reinterpret_cast<float *>(prow + j * 32 * 4);
                     if (ACC) v += *p;
-                    *p = v;
+                    __builtin_nontemporal_store(v, p);
                 }
             }
             // keep the scheduler from hoisting all 256 accumulator reads at once
@@ -418,7 +421,8 @@ struct TileSpace {
 // Inside the persistent tile loop the row offsets would otherwise be hoisted
 // out of the loop (they depend only on ldc) and all 256 accumulators copied to
 // VGPRs at once; the opaque row stride and the per-element AGPR reads keep the
-// epilogue streaming through a few registers.
+// epilogue streaming through a few registers.  Non-temporal stores, as in
+// store_tile.
 template <bool BF16OUT, bool ACC, bool CHECK>
 __device__ __forceinline__ void store_block(v16f (&acc)[4][4], uint8_t *cbase, uint32_t ldc_bytes, int rows_left,
                                             int cols_left)
@@ -443,10 +447,10 @@ __device__ __forceinline__ void store_block(v16f (&acc)[4][4], uint8_t *cbase, u
                 uint8_t *p = cbase + rb + j * 32 * esize;
                 if (BF16OUT) {
                     if (ACC) v += (float)*reinterpret_cast<__bf16 *>(p);
-                    *reinterpret_cast<__bf16 *>(p) = (__bf16)v;
+                    __builtin_nontemporal_store((__bf16)v, reinterpret_cast<__bf16 *>(p));
                 } else {
                     if (ACC) v += *reinterpret_cast<float *>(p);
-                    *reinterpret_cast<float *>(p) = v;
+                    __builtin_nontemporal_store(v, reinterpret_cast<float *>(p));
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
