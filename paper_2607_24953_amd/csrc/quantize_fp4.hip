@@ -52,6 +52,15 @@ constexpr int kTile = 128;          // tile rows
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f2v __attribute__((ext_vector_type(2)));
+typedef unsigned int u4v __attribute__((ext_vector_type(4)));
+
+// 16-byte streaming load: the input is read once, so it should not displace
+// cache lines that are reused
+__device__ __forceinline__ uint4 load_stream16(const void *p)
+{
+    const u4v v = __builtin_nontemporal_load(reinterpret_cast<const u4v *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 template <typename T>
 struct Elem;
@@ -167,7 +176,7 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 uint4 q = make_uint4(0u, 0u, 0u, 0u);
-                if (r0 + i < a.rows) q = *reinterpret_cast<const uint4 *>(xr);
+                if (r0 + i < a.rows) q = load_stream16(xr);
                 v[i][0] = q.x; v[i][1] = q.y; v[i][2] = q.z; v[i][3] = q.w;
                 xr += a.stride_r;
             }
@@ -190,8 +199,8 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
         for (int i = 0; i < 8; ++i) {
             uint4 q0 = make_uint4(0u, 0u, 0u, 0u), q1 = q0;
             if (r0 + i < a.rows) {
-                q0 = *reinterpret_cast<const uint4 *>(xr);
-                q1 = *reinterpret_cast<const uint4 *>(xr + 4);
+                q0 = load_stream16(xr);
+                q1 = load_stream16(xr + 4);
             }
             v[i][0] = q0.x; v[i][1] = q0.y; v[i][2] = q0.z; v[i][3] = q0.w;
             v[i][NV - 4] = q1.x; v[i][NV - 3] = q1.y; v[i][NV - 2] = q1.z; v[i][NV - 1] = q1.w;

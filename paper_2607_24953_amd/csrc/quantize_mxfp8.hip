@@ -24,6 +24,14 @@ namespace {
 constexpr int kTile = 128;
 
 typedef short s2v __attribute__((ext_vector_type(2)));
+typedef unsigned int u4v __attribute__((ext_vector_type(4)));
+
+// 16-byte streaming load (the input is read once)
+__device__ __forceinline__ uint4 load_stream16(const void *p)
+{
+    const u4v v = __builtin_nontemporal_load(reinterpret_cast<const u4v *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint32_t load_bits(const void *x, bool is_f32, int64_t idx)
@@ -71,8 +79,8 @@ __global__ __launch_bounds__(256) void mxfp8_quantize_kernel(const QuantArgs a)
         for (int i = 0; i < 8; ++i) {
             uint4 q0 = make_uint4(0u, 0u, 0u, 0u), q1 = q0;
             if (r0 + i < a.rows) {
-                q0 = *reinterpret_cast<const uint4 *>(xr);
-                if (F32) q1 = *reinterpret_cast<const uint4 *>(xr + 16);
+                q0 = load_stream16(xr);
+                if (F32) q1 = load_stream16(xr + 16);
             }
             v[i][0] = q0.x; v[i][1] = q0.y; v[i][2] = q0.z; v[i][3] = q0.w;
             if (F32) { v[i][NV - 4] = q1.x; v[i][NV - 3] = q1.y; v[i][NV - 2] = q1.z; v[i][NV - 1] = q1.w; }
