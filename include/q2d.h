@@ -47,7 +47,7 @@ extern "C" {
 typedef enum {
     Q2D_OK = 0,
     Q2D_EINVAL = 1,          /* bad argument: null pointer, size, stride, alignment, shape mismatch */
-    Q2D_EUNSUPPORTED = 2,    /* valid request this build does not implement (e.g. block != 32) */
+    Q2D_EUNSUPPORTED = 2,    /* valid request this build does not implement (e.g. block 16) */
     Q2D_ELAUNCH = 3          /* the HIP runtime rejected a kernel launch */
 } q2d_status;
 
@@ -79,6 +79,10 @@ typedef enum {
  *            entries up to roundup(rows,128)/32 written.  Every value in
  *            scales_t equals the one in scales: the transposition invariance.
  *   A nibble is sign << 3 | m with m indexing {0, .5, 1, 1.5, 2, 3, 4, 6}.
+ *   block 64 (64x64 blocks, the larger block of the block-size trade-off,
+ *   Table 4): the same buffers and the same 32-granular scale grids; the byte
+ *   of 64x64 block (I, J) fills the four entries (2I..2I+1, 2J..2J+1) that
+ *   exist, so every GEMM reads a block-64 tensor exactly as a block-32 one.
  *
  * MXFP8 (Sec. 3.2):
  *   codes    [rows][ld_codes] E4M3 bytes, scales [rows][ld_scales]: one scale
@@ -111,7 +115,7 @@ typedef enum {
  */
 typedef struct {
     int32_t fmt;             /* q2d_fmt */
-    int32_t block;           /* block edge; 32 */
+    int32_t block;           /* block edge: 32, or 64 for FP4_2D */
     int64_t rows, cols;      /* logical shape R x C */
     uint8_t *codes;    int64_t ld_codes;
     uint8_t *codes_t;  int64_t ld_codes_t;
@@ -124,7 +128,7 @@ typedef struct {
  * minimal leading dimensions; pointers set to NULL) and, if `bytes` is not
  * NULL, the byte sizes of its four buffers {codes, codes_t, scales, scales_t}.
  * Host only.  Q2D_EINVAL for rows or cols <= 0; Q2D_EUNSUPPORTED for a block
- * other than 32.
+ * other than 32, except 64 with FP4_2D.
  */
 q2d_status q2d_tensor_init(q2d_tensor *t, q2d_fmt fmt, int64_t rows, int64_t cols,
                            int32_t block, int64_t bytes[4]);
@@ -137,7 +141,8 @@ q2d_status q2d_tensor_init(q2d_tensor *t, q2d_fmt fmt, int64_t rows, int64_t col
  *          > 0).  Views are allowed: stride_c == 1 (row-major) and
  *          stride_r == 1 (a transposed view) take the fast path, other strides
  *          a slower element-wise path.
- * block    32.
+ * block    32 or 64 (64x64 blocks, Table 4); equal to out->block
+ *          (Q2D_EINVAL otherwise).
  * mode     Q2D_RTN or Q2D_SR.  For SR the 16 random bits of the element with
  *          storage index i = r*stride_r + c*stride_c are half (i & 1) of word
  *          (i & 7) >> 1 of Philox4x32-10 with counter (g lo, g hi, offset lo,
@@ -145,7 +150,7 @@ q2d_status q2d_tensor_init(q2d_tensor *t, q2d_fmt fmt, int64_t rows, int64_t col
  *          rounds up iff floor(2^16 * d / delta) + r16 >= 2^16 (d = distance to
  *          the grid point below, delta = grid spacing).  A transposed view
  *          therefore draws the same bits as the matrix it views.
- * out      descriptor from q2d_tensor_init(FP4_2D, rows, cols, 32) with device
+ * out      descriptor from q2d_tensor_init(FP4_2D, rows, cols, block) with device
  *          buffers attached; ld_* may exceed the minimum.  At least one of
  *          codes / codes_t must be set.  Buffers must be 16-byte aligned and
  *          leading dimensions multiples of 16 (codes) and 4 (scales).
@@ -189,7 +194,8 @@ q2d_status mxfp8_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t col
  * codes_t/scales_t; K = X.rows) when transX == 1.  M = rows of op(A),
  * N = rows of op(B); both must have the same K.  FP4_2D and FP4_1D operands
  * may be mixed (1D activations with 2D weights and gradients: App. C); MXFP8
- * pairs only with MXFP8.
+ * pairs only with MXFP8.  Block-64 FP4_2D operands are read as block-32 ones
+ * (their scale grids hold each 64x64 block's byte in all four entries).
  *   forward     Y  = X  W^T : q2d_gemm(X, 0, W, 0, ...)
  *   data grad   dX = dY W   : q2d_gemm(dY, 0, W, 1, ...)
  *   weight grad dW = dY^T X : q2d_gemm(dY, 1, X, 1, ...)
@@ -207,7 +213,8 @@ q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int tr
  * Y [T][N] (row-major, ldy = N, dtype y_dt).  The SR streams of X and W use
  * (seed, offset_x) and (seed, offset_w).  qX may be FP4_1D (the paper's
  * activation layout, App. C): X is then quantized with q2d_quantize_1d and the
- * backward pass's weight gradient reads its 32x1 copy.
+ * backward pass's weight gradient reads its 32x1 copy.  Each FP4_2D
+ * quantization uses its descriptor's block (32, or 64 for 64x64 blocks).
  */
 q2d_status q2d_linear_fwd(const void *X, const void *W, q2d_dtype dt, int64_t T, int64_t N,
                           int64_t K, q2d_round mode_x, q2d_round mode_w, uint64_t seed,
@@ -219,7 +226,8 @@ q2d_status q2d_linear_fwd(const void *X, const void *W, q2d_dtype dt, int64_t T,
  * into qdY (both orientations) and computes dX = dY W into dX [T][K] and
  * dW = dY^T X into dW [N][K], reusing the forward's qX and qW transposed with
  * their unchanged scales (the straight-through estimator passes dY through the
- * quantizer unchanged).  accumulate_dw: 1 adds into dW.
+ * quantizer unchanged).  accumulate_dw: 1 adds into dW.  dY is quantized with
+ * qdY's block.
  */
 q2d_status q2d_linear_bwd(const void *dY, q2d_dtype dt, const q2d_tensor *qX,
                           const q2d_tensor *qW, q2d_round mode_dy, uint64_t seed,
@@ -242,7 +250,8 @@ q2d_status q2d_linear_bwd(const void *dY, q2d_dtype dt, const q2d_tensor *qX,
  * q2d_grouped_tensor_init: layout of the padded form (rows = the capacity
  * roundup(rows + 127 * nseg, 128), cols as given); bytes[] as q2d_tensor_init.
  * Rows beyond the last segment's padded end are not written.  Q2D_EINVAL for
- * rows or cols <= 0 or nseg outside [1, 1024].
+ * rows or cols <= 0 or nseg outside [1, 1024]; Q2D_EUNSUPPORTED for a block
+ * other than 32.
  */
 q2d_status q2d_grouped_tensor_init(q2d_tensor *t, int64_t rows, int64_t cols, int32_t nseg,
                                    int32_t block, int64_t bytes[4]);

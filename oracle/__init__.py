@@ -245,21 +245,37 @@ def to_float64(x) -> np.ndarray:
 # ------------------------------------------------------------------ quantizers
 
 def quantize_fp4_2d(x, mode: str = "rtn", seed: int = 0, offset: int = 0,
-                    threads: int = 0, index_base: int = 0) -> dict:
+                    threads: int = 0, index_base: int = 0, block: int = BLOCK) -> dict:
     """2D-block FP4 quantization of a 2-D CPU tensor into both packed layouts.
 
     ``index_base`` is added to every storage index before it keys the random
-    stream (the grouped form uses the segment's first storage index)."""
+    stream (the grouped form uses the segment's first storage index).
+    ``block`` 64 (the larger block of the block-size trade-off, Table 4): the
+    blocks are 64 x 64 and the scale grids keep the 32-granular layout, the byte
+    of 64-block (i, j) in the four entries (2i .. 2i+1, 2j .. 2j+1)."""
     hold, ptr, dt, R, C, sr, sc = _as_input(x)
     lay = fp4_layout(R, C)
     out = {k: np.zeros(v, dtype=np.uint8) for k, v in lay.items()}
-    lib().or_quantize_fp4_2d(ptr, dt, R, C, sr, sc, int(index_base), BLOCK,
+    if block == BLOCK:
+        sc_buf, sct_buf = out["scales"], out["scales_t"]
+    else:
+        assert block == 64
+        nr, nc = -(-R // block), -(-C // block)
+        sc_buf, sct_buf = np.zeros((nr, nc), np.uint8), np.zeros((nc, nr), np.uint8)
+    lib().or_quantize_fp4_2d(ptr, dt, R, C, sr, sc, int(index_base), int(block),
                              1 if mode == "sr" else 0,
                              int(seed), int(offset),
                              out["codes"].ctypes.data, lay["codes"][1],
                              out["codes_t"].ctypes.data, lay["codes_t"][1],
-                             out["scales"].ctypes.data, lay["scales"][1],
-                             out["scales_t"].ctypes.data, lay["scales_t"][1], int(threads))
+                             sc_buf.ctypes.data, sc_buf.shape[1],
+                             sct_buf.ctypes.data, sct_buf.shape[1], int(threads))
+    if block != BLOCK:
+        for name, comp in (("scales", sc_buf), ("scales_t", sct_buf)):
+            g = out[name]
+            i = np.arange(g.shape[0]) // 2
+            j = np.arange(g.shape[1]) // 2
+            inside = j < comp.shape[1]
+            g[:, inside] = comp[i][:, j[inside]]
     out["rows"], out["cols"] = R, C
     return out
 

@@ -194,17 +194,19 @@ def q2d_gemm(A: QTensor, transA: int, B: QTensor, transB: int, out: torch.Tensor
 
 def q2d_linear_fwd(X: torch.Tensor, W: torch.Tensor, mode_x="rtn", mode_w="rtn", seed: int = 0,
                    offset_x: int = 0, offset_w: int = 1, y_dtype=torch.bfloat16,
-                   qX: QTensor | None = None, qW: QTensor | None = None, Y=None, fmt_x: int = FP4_2D):
+                   qX: QTensor | None = None, qW: QTensor | None = None, Y=None, fmt_x: int = FP4_2D,
+                   block: int = 32):
     """Y = Q(X) Q(W)^T; returns (Y, qX, qW) with both orientations kept.  fmt_x
-    FP4_1D quantizes X in 1D blocks (the activation placement of the paper)."""
+    FP4_1D quantizes X in 1D blocks (the activation placement of the paper);
+    block 64 gives the 2D-block operands 64 x 64 blocks."""
     _check_input(X)
     _check_input(W)
     T, K = X.shape
     N = W.shape[0]
     if not (X.is_contiguous() and W.is_contiguous()) or W.shape[1] != K or X.dtype != W.dtype:
         raise Q2DError("q2d_linear_fwd expects contiguous X [T,K] and W [N,K] of one dtype")
-    qX = qX or QTensor(fmt_x, T, K, X.device)
-    qW = qW or QTensor(FP4_2D, N, K, X.device)
+    qX = qX or QTensor(fmt_x, T, K, X.device, 32 if fmt_x == FP4_1D else block)
+    qW = qW or QTensor(FP4_2D, N, K, X.device, block)
     if Y is None:
         Y = torch.empty((T, N), dtype=y_dtype, device=X.device)
     _check(_lib.q2d_linear_fwd(X.data_ptr(), W.data_ptr(), _dtype_code(X.dtype), T, N, K,
@@ -217,14 +219,15 @@ def q2d_linear_fwd(X: torch.Tensor, W: torch.Tensor, mode_x="rtn", mode_w="rtn",
 def q2d_linear_bwd(dY: torch.Tensor, qX: QTensor, qW: QTensor, mode_dy="sr", seed: int = 0,
                    offset_dy: int = 2, dx_dtype=torch.bfloat16, dw_dtype=torch.float32,
                    dW: torch.Tensor | None = None, accumulate_dw: bool = False,
-                   qdY: QTensor | None = None, dX=None):
-    """dX = Q(dY) Q(W), dW = Q(dY)^T Q(X) reusing the forward's operands; returns (dX, dW, qdY)."""
+                   qdY: QTensor | None = None, dX=None, block: int = 32):
+    """dX = Q(dY) Q(W), dW = Q(dY)^T Q(X) reusing the forward's operands; returns
+    (dX, dW, qdY).  block: dY's block edge (32, or 64 for 64 x 64 blocks)."""
     _check_input(dY)
     T, N = dY.shape
     K = qX.cols
     if not dY.is_contiguous():
         raise Q2DError("q2d_linear_bwd expects a contiguous dY")
-    qdY = qdY or QTensor(FP4_2D, T, N, dY.device)
+    qdY = qdY or QTensor(FP4_2D, T, N, dY.device, block)
     if dX is None:
         dX = torch.empty((T, K), dtype=dx_dtype, device=dY.device)
     if dW is None:

@@ -60,7 +60,7 @@ q2d_status check_tensor(const q2d_tensor *t, q2d_fmt fmt, int64_t R, int64_t C)
 {
     if (!t) return Q2D_EINVAL;
     if (t->fmt != fmt || t->rows != R || t->cols != C) return Q2D_EINVAL;
-    if (t->block != 32) return Q2D_EUNSUPPORTED;
+    if (t->block != 32 && !(t->block == 64 && fmt == Q2D_FMT_FP4_2D)) return Q2D_EUNSUPPORTED;
     if (!t->codes && !t->codes_t) return Q2D_EINVAL;
     const Layout l = layout_of(fmt, R, C);
     if (!check_pair(t->codes, t->ld_codes, l.ld_codes, t->scales, t->ld_scales, l.ld_scales)) return Q2D_EINVAL;
@@ -101,6 +101,7 @@ QuantArgs make_quant_args(const void *x, int64_t R, int64_t C, int64_t sr, int64
     a.seg_offsets = nullptr;
     a.nseg = 0;
     a.store_rows = a.rows;
+    a.block = 32;
     return a;
 }
 
@@ -127,7 +128,9 @@ q2d_status q2d_tensor_init(q2d_tensor *t, q2d_fmt fmt, int64_t rows, int64_t col
 {
     if (!t || rows <= 0 || cols <= 0) return Q2D_EINVAL;
     if (fmt != Q2D_FMT_FP4_2D && fmt != Q2D_FMT_MXFP8 && fmt != Q2D_FMT_FP4_1D) return Q2D_EINVAL;
-    if (block != 32) return Q2D_EUNSUPPORTED;
+    // 64 x 64 blocks keep the 32-granular scale grid (each block's byte in its
+    // four entries), so every GEMM reads them unchanged
+    if (block != 32 && !(block == 64 && fmt == Q2D_FMT_FP4_2D)) return Q2D_EUNSUPPORTED;
     const Layout l = layout_of(fmt, rows, cols);
     t->fmt = fmt; t->block = block; t->rows = rows; t->cols = cols;
     t->codes = t->codes_t = t->scales = t->scales_t = nullptr;
@@ -149,10 +152,12 @@ q2d_status q2d_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols,
     q2d_status s = check_input(x, dt, rows, cols, stride_r, stride_c);
     if (s != Q2D_OK) return s;
     if (mode != Q2D_RTN && mode != Q2D_SR) return Q2D_EINVAL;
-    if (block != 32) return Q2D_EUNSUPPORTED;
+    if (block != 32 && block != 64) return Q2D_EUNSUPPORTED;
     s = check_tensor(out, Q2D_FMT_FP4_2D, rows, cols);
     if (s != Q2D_OK) return s;
-    const QuantArgs a = make_quant_args(x, rows, cols, stride_r, stride_c, seed, offset, out);
+    if (out->block != block) return Q2D_EINVAL;
+    QuantArgs a = make_quant_args(x, rows, cols, stride_r, stride_c, seed, offset, out);
+    a.block = block;
     if (launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, false, stream) != hipSuccess) return Q2D_ELAUNCH;
     return Q2D_OK;
 }
@@ -167,6 +172,7 @@ q2d_status q2d_quantize_1d(const void *x, q2d_dtype dt, int64_t rows, int64_t co
     if (block != 32) return Q2D_EUNSUPPORTED;
     s = check_tensor(out, Q2D_FMT_FP4_1D, rows, cols);
     if (s != Q2D_OK) return s;
+    if (out->block != 32) return Q2D_EUNSUPPORTED;
     // a transposed view's rowwise blocks are its storage's column blocks: the
     // swap of make_quant_args sends each copy to the right buffers
     const QuantArgs a = make_quant_args(x, rows, cols, stride_r, stride_c, seed, offset, out);
@@ -192,7 +198,7 @@ q2d_status mxfp8_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t col
     a.scales_t = out->scales_t; a.ld_scales_t = out->ld_scales_t;
     a.rows_pad = rup(rows, 128); a.cols_pad = rup(cols, 128);
     a.nbr = rows; a.nbc = cols;
-    a.seg_offsets = nullptr; a.nseg = 0; a.store_rows = rows;
+    a.seg_offsets = nullptr; a.nseg = 0; a.store_rows = rows; a.block = 32;
     if (launch_mxfp8_quantize(a, dtype_bytes(dt), stream) != hipSuccess) return Q2D_ELAUNCH;
     return Q2D_OK;
 }
@@ -207,7 +213,11 @@ q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int tr
     const bool fp4a = A->fmt == Q2D_FMT_FP4_2D || A->fmt == Q2D_FMT_FP4_1D;
     const bool fp4b = B->fmt == Q2D_FMT_FP4_2D || B->fmt == Q2D_FMT_FP4_1D;
     if (!(fp4a && fp4b) && !(A->fmt == Q2D_FMT_MXFP8 && B->fmt == Q2D_FMT_MXFP8)) return Q2D_EINVAL;
-    if (A->block != 32 || B->block != 32) return Q2D_EUNSUPPORTED;
+    // FP4_2D operands may have 64 x 64 blocks (scales stored 32-granular)
+    auto block_ok = [](const q2d_tensor *t) {
+        return t->block == 32 || (t->block == 64 && t->fmt == Q2D_FMT_FP4_2D);
+    };
+    if (!block_ok(A) || !block_ok(B)) return Q2D_EUNSUPPORTED;
     if (A->rows <= 0 || A->cols <= 0 || B->rows <= 0 || B->cols <= 0) return Q2D_EINVAL;
     const int64_t M = transA ? A->cols : A->rows, Ka = transA ? A->rows : A->cols;
     const int64_t N = transB ? B->cols : B->rows, Kb = transB ? B->rows : B->cols;
@@ -253,9 +263,9 @@ q2d_status q2d_linear_fwd(const void *X, const void *W, q2d_dtype dt, int64_t T,
     if (!qX || !qW || !qX->codes || !qW->codes) return Q2D_EINVAL;
     q2d_status s = qX->fmt == Q2D_FMT_FP4_1D
                        ? q2d_quantize_1d(X, dt, T, K, K, 1, 32, mode_x, seed, offset_x, qX, stream)
-                       : q2d_quantize(X, dt, T, K, K, 1, 32, mode_x, seed, offset_x, qX, stream);
+                       : q2d_quantize(X, dt, T, K, K, 1, qX->block, mode_x, seed, offset_x, qX, stream);
     if (s != Q2D_OK) return s;
-    s = q2d_quantize(W, dt, N, K, K, 1, 32, mode_w, seed, offset_w, qW, stream);
+    s = q2d_quantize(W, dt, N, K, K, 1, qW->block, mode_w, seed, offset_w, qW, stream);
     if (s != Q2D_OK) return s;
     return q2d_gemm(qX, 0, qW, 0, Y, y_dt, N, 0, stream);
 }
@@ -268,7 +278,7 @@ q2d_status q2d_linear_bwd(const void *dY, q2d_dtype dt, const q2d_tensor *qX, co
     const int64_t T = qX->rows, K = qX->cols, N = qW->rows;
     if (qW->cols != K || qdY->rows != T || qdY->cols != N) return Q2D_EINVAL;
     if (!qdY->codes || !qdY->codes_t || !qX->codes_t || !qW->codes_t) return Q2D_EINVAL;
-    q2d_status s = q2d_quantize(dY, dt, T, N, N, 1, 32, mode_dy, seed, offset_dy, qdY, stream);
+    q2d_status s = q2d_quantize(dY, dt, T, N, N, 1, qdY->block, mode_dy, seed, offset_dy, qdY, stream);
     if (s != Q2D_OK) return s;
     s = q2d_gemm(qdY, 0, qW, 1, dX, dx_dt, K, 0, stream);
     if (s != Q2D_OK) return s;
@@ -279,6 +289,7 @@ q2d_status q2d_grouped_tensor_init(q2d_tensor *t, int64_t rows, int64_t cols, in
                                    int64_t bytes[4])
 {
     if (nseg <= 0 || nseg > kMaxGroups || rows <= 0) return Q2D_EINVAL;
+    if (block != 32) return Q2D_EUNSUPPORTED;
     return q2d_tensor_init(t, Q2D_FMT_FP4_2D, grouped_capacity(rows, nseg), cols, block, bytes);
 }
 
@@ -296,6 +307,7 @@ q2d_status q2d_grouped_quantize(const void *x, q2d_dtype dt, int64_t rows, int64
     const int64_t cap = grouped_capacity(rows, nseg);
     s = check_tensor(out, Q2D_FMT_FP4_2D, cap, cols);
     if (s != Q2D_OK) return s;
+    if (out->block != 32) return Q2D_EUNSUPPORTED;
     QuantArgs a = make_quant_args(x, rows, cols, stride_r, 1, seed, offset, out);
     a.rows_pad = cap;               // grid bound over padded rows
     a.seg_offsets = seg_offsets;

@@ -249,7 +249,6 @@ constexpr int BM2 = 256, BN2 = 256;
 constexpr int kStages = 4;
 constexpr int kDmaPerTile = 9;      // per wave: 4 for A, 4 for B, 1 for the scale words
 constexpr int kCodeBytes = BM2 * 64;                  // 16 KB per operand per stage
-constexpr int kStageBytes = 2 * kCodeBytes + 1024;    // + 4 waves x 256 B of scale words
 
 // Wave-uniform 64-bit value (moves it to SGPRs).
 __device__ __forceinline__ uint64_t uniform64(uint64_t v)
@@ -470,7 +469,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     constexpr int RB = F::kRowBytes;                // 64
     constexpr bool A1 = (SM & 1) != 0, B1 = (SM & 2) != 0;
     constexpr int kDma = kDmaPerTile + A1 + B1;     // 9 .. 11
-    constexpr int kWordsA1 = 2 * kCodeBytes + 1024;             // per-row A scale words
+    constexpr int kWordsA1 = 2 * kCodeBytes + 1024;             // after 2 x codes + 1 KB of 2D scale words: per-row A scale words
     constexpr int kWordsB1 = kWordsA1 + (A1 ? 1024 : 0);       // per-row B scale words
     constexpr int kStageBytes = kWordsB1 + (B1 ? 1024 : 0);
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];

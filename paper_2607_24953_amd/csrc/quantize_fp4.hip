@@ -277,6 +277,15 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
             cm[j] = max(cm[j], (uint32_t)__shfl_xor((int)cm[j], 32));
         }
     }
+    if (!ONED && !GROUPED && a.block == 64) {
+        // 64 x 64 blocks: the 32 x 32 block beside it in this wave (lane bit 2), then
+        // the 32-row strip of the paired wave through LDS
+        __shared__ uint32_t am64[4][2 * WC];
+        am = max(am, (uint32_t)__shfl_xor((int)am, 4));
+        if (rg == 0 && (cc & 7) == 0) am64[wr][wc * 2 + (cc >> 3)] = am;
+        __syncthreads();
+        am = max(am, am64[wr ^ 1][wc * 2 + (cc >> 3)]);
+    }
     const bool finite = am < 0x7F800000u;
     const int e = fp4_block_exponent(am);
     const float scale = bits_f((uint32_t)(127 + e) << 23);       // 2^e

@@ -70,7 +70,8 @@ def test_error_paths(q2d):
     assert L.q2d_quantize(fake, 1, 65, 64, 64, 1, 32, 0, 0, 0, ctypes.byref(d), None) == 1
     assert L.q2d_quantize(fake, 1, 64, 64, 0, 1, 32, 0, 0, 0, ctypes.byref(d), None) == 1
     assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 32, 9, 0, 0, ctypes.byref(d), None) == 1
-    assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 64, 0, 0, 0, ctypes.byref(d), None) == 2
+    assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 16, 0, 0, 0, ctypes.byref(d), None) == 2
+    assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 64, 0, 0, 0, ctypes.byref(d), None) == 1   # != out->block
     assert L.q2d_quantize(fake + 1, 1, 64, 64, 64, 1, 32, 0, 0, 0, ctypes.byref(d), None) == 1
     # misaligned code buffer and too-small leading dimension
     d.codes = fake + 8
@@ -105,6 +106,34 @@ def test_error_paths(q2d):
     assert L.q2d_gemm(ctypes.byref(h), 0, ctypes.byref(f), 0, fake, 0, 64, 0, None) == 1
     assert L.q2d_gemm(ctypes.byref(f), 0, ctypes.byref(h), 0, fake, 0, 64, 0, None) == 1
     assert q2d.q2d_status_string(2) == "unsupported configuration"
+
+
+def test_block64_descriptors(q2d):
+    """64 x 64 blocks: FP4_2D only, the block-32 layout (32-granular scale grids);
+    the quantizer needs the descriptor's block; 1D and grouped stay at 32."""
+    import oracle
+    L = q2d._lib
+    sizes = (ctypes.c_int64 * 4)()
+    fake = 0x1000
+    d = q2d._Tensor()
+    for R, C in ((100, 70), (4096, 11008)):
+        assert L.q2d_tensor_init(ctypes.byref(d), 0, R, C, 64, sizes) == 0
+        lay = oracle.fp4_layout(R, C)
+        assert d.block == 64 and (d.ld_codes, d.ld_codes_t, d.ld_scales, d.ld_scales_t) == (
+            lay["codes"][1], lay["codes_t"][1], lay["scales"][1], lay["scales_t"][1])
+    assert L.q2d_tensor_init(ctypes.byref(d), 1, 64, 64, 64, sizes) == 2    # MXFP8
+    assert L.q2d_tensor_init(ctypes.byref(d), 2, 64, 64, 64, sizes) == 2    # FP4_1D
+    assert L.q2d_tensor_init(ctypes.byref(d), 0, 64, 64, 128, sizes) == 2
+    assert L.q2d_grouped_tensor_init(ctypes.byref(d), 300, 64, 4, 64, sizes) == 2
+    assert L.q2d_tensor_init(ctypes.byref(d), 0, 64, 64, 64, sizes) == 0
+    d.codes, d.scales, d.codes_t, d.scales_t = fake, fake, fake, fake
+    assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 32, 0, 0, 0, ctypes.byref(d), None) == 1   # != out->block
+    assert L.q2d_quantize_1d(fake, 1, 64, 64, 64, 1, 64, 0, 0, 0, ctypes.byref(d), None) == 2
+    # a block-64 operand is no MXFP8 partner
+    f = q2d._Tensor()
+    assert L.q2d_tensor_init(ctypes.byref(f), 1, 64, 64, 32, sizes) == 0
+    f.codes, f.scales, f.codes_t, f.scales_t = fake, fake, fake, fake
+    assert L.q2d_gemm(ctypes.byref(d), 0, ctypes.byref(f), 0, fake, 0, 64, 0, None) == 1
 
 
 @pytest.mark.parametrize("counts,C", [([0, 1, 31, 33, 127, 130], 96), ([256], 128),

@@ -168,3 +168,56 @@ def test_grouped_segments_are_independent_matrices():
             np.testing.assert_array_equal(g["codes_t"][:, p[e] // 2:p[e] // 2 + rows_t],
                                           seg["codes_t"])
             assert not g["codes"][p[e] + n:p[e + 1]].any()
+
+
+# ------------------------------------------------------------------ 64 x 64 blocks (Table 4)
+
+def _expand64(M64, nrows, ncols):
+    """32-granular grid holding the byte of 64-block (i // 2, j // 2); 0 past the blocks."""
+    g = np.zeros((nrows, ncols), dtype=M64.dtype)
+    for i in range(nrows):
+        for j in range(ncols):
+            if i // 2 < M64.shape[0] and j // 2 < M64.shape[1]:
+                g[i, j] = M64[i // 2, j // 2]
+    return g
+
+
+@pytest.mark.parametrize("shape", [(128, 192), (100, 70), (33, 129), (257, 31)])
+@pytest.mark.parametrize("mode", ["rtn", "sr"])
+def test_block64_elementwise_definition(shape, mode):
+    x = synth.normal(shape, 0.7, 31, torch.bfloat16)
+    q = oracle.quantize_fp4_2d(x, mode, seed=5, offset=9, block=64)
+    x64 = oracle.to_float64(x)
+    R, C = shape
+    e64 = np.vectorize(oracle.fp4_scale_exponent)(_block_max(x64, 64)).astype(np.int64)
+    lay = oracle.fp4_layout(R, C)
+    np.testing.assert_array_equal(q["scales"], _expand64((e64 + 127).astype(np.uint8), *lay["scales"]))
+    np.testing.assert_array_equal(q["scales_t"], _expand64((e64.T + 127).astype(np.uint8), *lay["scales_t"]))
+    eb = e64[np.arange(R)[:, None] // 64, np.arange(C)[None, :] // 64]
+    idx = np.arange(R)[:, None] * x.stride(0) + np.arange(C)[None, :]
+    r16 = np.vectorize(lambda i: oracle.sr_bits(int(i), 5, 9))(idx).astype(np.uint32) if mode == "sr" else None
+    want = oracle.fp4_codes(x64, eb, mode == "sr", r16)
+    np.testing.assert_array_equal(_unpack(q["codes"], C), want)
+    np.testing.assert_array_equal(_unpack(q["codes_t"], R), want.T)
+
+
+@pytest.mark.parametrize("mode", ["rtn", "sr"])
+def test_block64_transposed_view_swaps_layouts(mode):
+    x = synth.normal((150, 200), 1.0, 32, torch.bfloat16)
+    q = oracle.quantize_fp4_2d(x, mode, 3, 4, block=64)
+    qt = oracle.quantize_fp4_2d(x.t(), mode, 3, 4, block=64)
+    for a, b in (("codes", "codes_t"), ("scales", "scales_t")):
+        np.testing.assert_array_equal(qt[a], q[b])
+        np.testing.assert_array_equal(qt[b], q[a])
+
+
+def test_block64_reduces_to_block32_when_subblock_maxima_agree():
+    """If the four 32 x 32 sub-blocks of every 64 x 64 block share one maximum, both
+    block sizes give the same scales and codes."""
+    x = synth.normal((192, 256), 0.5, 33, torch.float32)
+    x = torch.clamp(x, -3.0, 3.0)
+    x[::32, ::32] = 7.0
+    q32 = oracle.quantize_fp4_2d(x, "rtn")
+    q64 = oracle.quantize_fp4_2d(x, "rtn", block=64)
+    for k in ("codes", "codes_t", "scales", "scales_t"):
+        np.testing.assert_array_equal(q64[k], q32[k])
