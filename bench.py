@@ -50,6 +50,9 @@ WORKLOAD_TEXT = {
                    "quantization placement: activations X in 1D FP4 (1x32 blocks for the forward "
                    "GEMM, 32x1 for the weight gradient), W and dY in 32x32 2D-block FP4 (X, W "
                    "round-to-nearest; dY stochastic)",
+    "dense_7b_b64": "7B-class dense linears fwd+bwd (shapes and tensors of dense_7b) with 64x64 "
+                    "2D-block FP4 for X, W and dY (the larger block of the block-size trade-off; "
+                    "X, W round-to-nearest; dY stochastic)",
     "mixed_7b": "7B-class block fwd+bwd, tokens 16384: Q/K projections in MXFP8 (E4M3, 1x32) "
                 "and V, O, gate, up, down in 32x32 2D-block FP4 with stochastic rounding; "
                 "bf16 inputs with outlier channels",
@@ -76,7 +79,7 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="dense_7b", choices=sorted(WORKLOAD_TEXT))
-    p.add_argument("--also", default="moe_30b,mixed_7b,dense_7b_1d",
+    p.add_argument("--also", default="moe_30b,mixed_7b,dense_7b_1d,dense_7b_b64",
                    help="further workloads measured in the same run (comma list, or 'none')")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-tokens", type=int, default=256)
@@ -217,12 +220,12 @@ class Step:
                     self.ops.append(("quant_mxfp8", name + ".mxfp8", b, b,
                                      lambda t=t, o=qt[key]: q2d.mxfp8_quantize(t, out=o)))
                 else:
-                    qt[key] = q2d.QTensor(q2d.FP4_2D, t.shape[0], t.shape[1], dev)
+                    qt[key] = q2d.QTensor(q2d.FP4_2D, t.shape[0], t.shape[1], dev, w.block)
                     off = len(qt)
                     b = quant_bytes(t)
                     self.ops.append(("quant_fp4", name, b, b,
                                      lambda t=t, o=qt[key], m=w.rounding[name], off=off:
-                                     q2d.q2d_quantize(t, m, w.seed, off, out=o)))
+                                     q2d.q2d_quantize(t, m, w.seed, off, out=o, block=w.block)))
         for lin in w.linears:
             x1d = fmt_of(lin, lin.x) == "fp4_1d"
             qx, qw, qdy = qt[(lin.x, fmt_of(lin, lin.x))], qt[(lin.w, lin.fmt)], qt[(lin.dy, lin.fmt)]
@@ -316,7 +319,8 @@ def measure(step, torch, steps: int, warmup: int) -> dict:
         n[1] += ms; n[2] += work; n[3] += 1
     ms_per_step = wall * 1e3 / steps
     res = {"ms_per_step": ms_per_step, "value": step.flops / (ms_per_step * 1e-3) / 1e12,
-           "kinds": {}, "per_kernel": {}}
+           "kinds": {}, "per_kernel": {},
+           "launches": len(step.ops) * (warmup + 2 * steps)}      # one dispatch per op
     for kind, (ms, work, n, abytes) in kinds.items():
         bound, peak, unit = KIND_PEAK[kind]
         scale = 1e12 if unit == "TFLOP/s" else 1e9
@@ -364,19 +368,20 @@ def cpu_baseline(w, tokens: int):
                       "%.3f TFLOP" % (len(w.linears), tokens, dt, flops / 1e12)}
 
 
-PROFILE_WORKLOADS = ("dense_7b", "moe_30b", "mixed_7b", "dense_7b_1d")
+PROFILE_WORKLOADS = ("dense_7b", "moe_30b", "mixed_7b", "dense_7b_1d", "dense_7b_b64")
 PROFILE_FILES = {
     "dense_7b": [("gemm_fp4_persistent_kernel.dense_7b.md", ("gemm_fp4",)),
                  ("fp4_quantize_kernel.dense_7b.md", ("quant_fp4",))],
     "moe_30b": [("grouped_fp4_kernels.moe_30b.md", ("gemm_fp4_grouped", "quant_fp4_grouped", "quant_fp4"))],
     "dense_7b_1d": [("fp4_1d_kernels.dense_7b_1d.md", ("quant_fp4_1d", "gemm_fp4", "quant_fp4"))],
     "mixed_7b": [("mxfp8_kernels.mixed_7b.md", ("gemm_fp8", "quant_mxfp8", "gemm_fp4", "quant_fp4"))],
+    "dense_7b_b64": [("block64_kernels.dense_7b_b64.md", ("quant_fp4", "gemm_fp4"))],
 }
 PROFILE_COMMANDS = """cd /tmp && export TMPDIR=/tmp; R=/root/repo; O=$R/gpurun_out/pb
 rocprofv3 --kernel-trace --stats --output-format csv -d $O/trace -o bench -- python3 $R/bench.py > $O/bench_trace.log 2>&1
 for c in FETCH_SIZE WRITE_SIZE; do
   rocprofv3 --pmc $c --output-format csv -d $O/copy_$c -o copy -- python3 $R/bench.py --copy-calibration 1073741824 > $O/copy_$c.log 2>&1
-  for wl in dense_7b moe_30b mixed_7b dense_7b_1d; do
+  for wl in dense_7b moe_30b mixed_7b dense_7b_1d dense_7b_b64; do
     rocprofv3 --pmc $c --output-format csv -d $O/${wl}_$c -o $wl -- python3 $R/bench.py --workload $wl --also none --steps 1 --warmup 0 --no-cpu-baseline > $O/${wl}_$c.log 2>&1
   done
 done
@@ -445,27 +450,24 @@ def summarize_profiles(d: str, out_dir: str):
         json.dump(traffic, f, indent=1, sort_keys=True)
         f.write("\n")
 
-    # kernel trace of the default benchmark run: dispatches split by workload phase
-    # (the workloads run in order; the first grouped launch starts the MoE phase, the
-    # first MXFP8 launch the mixed phase and the first 1D quantization the phase of
-    # the 7B linears with 1D activations)
+    # kernel trace of the default benchmark run: the workloads run in order, each
+    # making a known number of libq2d dispatches, which splits the trace by workload
     bt = _json_line(os.path.join(d, "bench_trace.log"))
     events = {bt["config"]["name"]: bt["kinds"]}
+    phases = [(bt["config"]["name"], bt["launches"])]
     for wl, o in bt.get("other_workloads", {}).items():
         events[wl] = o["kinds"]
+        phases.append((wl, o["launches"]))
     rows = _csv(os.path.join(d, "trace"), "_kernel_trace.csv")
     rows.sort(key=lambda r: int(r["Dispatch_Id"]))
-    phase, durs = "dense_7b", {}
-    for r in rows:
+    rows = [r for r in rows if kind_of(r["Kernel_Name"]) is not None]
+    if len(rows) != sum(n for _, n in phases):
+        raise ValueError("trace holds %d libq2d dispatches, the run reports %d"
+                         % (len(rows), sum(n for _, n in phases)))
+    owner = [wl for wl, n in phases for _ in range(n)]
+    durs = {}
+    for r, phase in zip(rows, owner):
         kind = kind_of(r["Kernel_Name"])
-        if kind is None:
-            continue
-        if kind.endswith("grouped") and phase == "dense_7b":
-            phase = "moe_30b"
-        if kind.endswith("mxfp8") or kind == "gemm_fp8":
-            phase = "mixed_7b"
-        if kind == "quant_fp4_1d":
-            phase = "dense_7b_1d"
         a = durs.setdefault((phase, kind), [0.0, 0])
         a[0] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-6; a[1] += 1
     stats = _csv(os.path.join(d, "trace"), "_kernel_stats.csv")
@@ -553,11 +555,12 @@ def main():
                    "gemms_per_step": sum(1 for o in step.ops if o[0].startswith("gemm")),
                    "gemm_tflop_per_step": step.flops / 1e12,
                    "quantizations_per_step": sum(1 for o in step.ops if o[0].startswith("quant")),
-                   "block": 32},
+                   "block": w.block},
         "roofline": roof,
         "quantizer": quant,
         "kinds": kinds,
         "per_kernel": res["per_kernel"],
+        "launches": res["launches"],
         "source_hashes": {k: kind_hash(k) for k in kinds},
     }
     others = [a for a in args.also.split(",") if a and a != "none" and a != args.workload]
@@ -574,7 +577,7 @@ def main():
             rec["other_workloads"][name] = {
                 "workload": WORKLOAD_TEXT[name], "TFLOP/s": round(ro["value"], 2),
                 "ms_per_step": round(ro["ms_per_step"], 4), "gemm_tflop_per_step": so.flops / 1e12,
-                "kinds": ro["kinds"], "per_kernel": ro["per_kernel"]}
+                "kinds": ro["kinds"], "per_kernel": ro["per_kernel"], "launches": ro["launches"]}
             del so, wo
             torch.cuda.empty_cache()
     if not args.no_cpu_baseline:

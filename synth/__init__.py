@@ -28,7 +28,7 @@ import torch
 
 __all__ = [
     "normal", "add_outlier_channels", "moe_counts", "segment_offsets",
-    "Workload", "tiny", "dense_1b", "dense_7b", "dense_7b_1d", "moe_30b", "mixed_7b", "WORKLOADS",
+    "Workload", "tiny", "dense_1b", "dense_7b", "dense_7b_1d", "dense_7b_b64", "moe_30b", "mixed_7b", "WORKLOADS",
 ]
 
 
@@ -113,6 +113,7 @@ class Workload:
     rounding: dict = field(default_factory=dict)    # tensor name -> "rtn" | "sr"
     seed: int = 0                                   # Philox seed for SR
     extra: dict = field(default_factory=dict)
+    block: int = 32                                 # 2D block edge (32, or 64)
 
     @property
     def gemm_flops(self) -> int:
@@ -193,6 +194,15 @@ def dense_7b_1d(device="cpu") -> Workload:
     return w
 
 
+def dense_7b_b64(device="cpu") -> Workload:
+    """The dense_7b tensors and linears with 64 x 64 blocks for X, W and dY (the larger
+    block of the block-size trade-off, Table 4)."""
+    w = dense_7b(device)
+    w.block = 64
+    w.name = "dense_7b_b64"
+    return w
+
+
 def mixed_7b(device="cpu") -> Workload:
     """7B block with Q/K projections in MXFP8 and V, O, gate, up, down in 2D-block FP4 (SR)."""
     T, H, F = 16384, 4096, 11008
@@ -235,4 +245,4 @@ def moe_30b(device="cpu", tokens: int = 16384, experts: int = 128, topk: int = 8
 
 
 WORKLOADS = {"tiny": tiny, "dense_1b": dense_1b, "dense_7b": dense_7b, "dense_7b_1d": dense_7b_1d,
-             "moe_30b": moe_30b, "mixed_7b": mixed_7b}
+             "dense_7b_b64": dense_7b_b64, "moe_30b": moe_30b, "mixed_7b": mixed_7b}
