@@ -235,6 +235,32 @@ q2d_status q2d_linear_bwd(const void *dY, q2d_dtype dt, const q2d_tensor *qX,
                           void *dW, q2d_dtype dw_dt, int accumulate_dw, hipStream_t stream);
 
 /*
+ * Dequantization of one stored copy (Sec. 2, "Bias induced by scale
+ * inconsistency"; Fig. 1): the R x C values that a GEMM reading that copy
+ * multiplies, in the matrix's own orientation.  copy 0 reads codes/scales (the
+ * copy the forward GEMM reads), copy 1 reads codes_t/scales_t (the copy the
+ * backward GEMMs read), both mapped back to element (r, c).  For FP4_2D the two
+ * copies give identical output (transposition invariance); for FP4_1D and
+ * MXFP8 they differ where the rowwise and columnwise blocks have different
+ * scales.
+ *
+ * t        any descriptor from q2d_tensor_init (FP4_2D with block 32 or 64,
+ *          FP4_1D, MXFP8) whose chosen copy has buffers attached.
+ * out      device pointer, row-major [rows][ldo] (ldo >= cols, elements) of
+ *          out_dt.  Q2D_F32: the exact value code * 2^e (E2M1 or E4M3FN code),
+ *          rounded once to nearest even only outside float32's range;
+ *          Q2D_BF16: round to nearest even of that value.  A block with scale
+ *          byte 0xFF, and an E4M3 NaN code, give NaN.
+ * exps     optional (NULL to skip) device int8 [rows][lde] (lde >= cols): the
+ *          scale exponent e of each element's block, -128 for scale byte 0xFF.
+ *          exps of copy 0 minus exps of copy 1 is the scale-difference map.
+ * Q2D_EINVAL for a missing buffer, copy not 0 or 1, or leading dimensions
+ * below cols.  Stream-ordered; no host synchronisation.
+ */
+q2d_status q2d_dequantize(const q2d_tensor *t, int copy, void *out, q2d_dtype out_dt, int64_t ldo,
+                          int8_t *exps, int64_t lde, hipStream_t stream);
+
+/*
  * Grouped (mixture-of-experts) form.  The rows of x are nseg expert segments
  * stored back to back: segment e is rows seg_offsets[e] .. seg_offsets[e+1]
  * (seg_offsets: device array of nseg + 1 int64, ascending, seg_offsets[0] = 0,

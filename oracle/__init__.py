@@ -384,6 +384,7 @@ def dequant_mxfp8(codes: np.ndarray, scales: np.ndarray, R: int, C: int) -> np.n
     m = b & 7
     mag = np.where(E == 0, np.ldexp(m.astype(np.float64), -9),
                    np.ldexp(1.0 + m / 8.0, (E - 7)))
+    mag = np.where((b & 0x7F) == 0x7F, np.nan, mag)        # E4M3FN: S.1111.111 is NaN
     val = np.where(b & 0x80, -mag, mag)
     s = _scale_values(scales[:R])
     return val * s[:, np.arange(C) // 32]
@@ -404,6 +405,34 @@ def operand(q: dict, transpose: bool, fmt: str = "fp4") -> np.ndarray:
     if not transpose:
         return dequant_mxfp8(q["codes"], q["scales"], R, C)
     return dequant_mxfp8(q["codes_t"], q["scales_t"], C, R)
+
+
+def dequantize(q: dict, copy: int, fmt: str = "fp4") -> np.ndarray:
+    """R x C float64 values of one stored copy (0: codes/scales, the copy the
+    forward GEMM reads; 1: codes_t/scales_t, the backward GEMMs' copy) in the
+    matrix's own orientation: the quantized operands X_fwd and X_bwd of Sec. 2
+    ("Bias induced by scale inconsistency")."""
+    return operand(q, False, fmt) if copy == 0 else operand(q, True, fmt).T
+
+
+def scale_exponents(q: dict, copy: int, fmt: str = "fp4") -> np.ndarray:
+    """R x C int64 scale exponent e of each element's block in one stored copy
+    (-128 for scale byte 0xFF); copy 0 minus copy 1 is the scale-difference map
+    of Fig. 1."""
+    R, C = q["rows"], q["cols"]
+    if copy == 0:
+        K, S, sc = C, R, q["scales"]
+    else:
+        K, S, sc = R, C, q["scales_t"]
+    if fmt == "fp4":
+        g = sc[:(S + BLOCK - 1) // BLOCK]
+        e = g[np.arange(S) // BLOCK][:, np.arange(K) // BLOCK]
+    elif fmt == "fp4_1d":
+        e = scale_grid_1d(sc, S)[:, np.arange(K) // 32]
+    else:
+        e = sc[:S][:, np.arange(K) // 32]
+    e = np.where(e == 0xFF, -128, e.astype(np.int64) - 127)
+    return e if copy == 0 else e.T
 
 
 def gemm(a: np.ndarray, b: np.ndarray) -> np.ndarray:

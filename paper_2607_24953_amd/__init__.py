@@ -17,7 +17,7 @@ __all__ = [
     "Q2DError", "QTensor", "RTN", "SR", "FP4_2D", "MXFP8", "FP4_1D", "lib_path",
     "q2d_tensor_init", "q2d_quantize", "q2d_quantize_1d", "mxfp8_quantize", "q2d_gemm",
     "q2d_linear_fwd", "q2d_linear_bwd", "q2d_grouped_tensor_init", "q2d_grouped_quantize",
-    "q2d_grouped_gemm", "q2d_status_string",
+    "q2d_grouped_gemm", "q2d_dequantize", "q2d_status_string",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -58,11 +58,12 @@ def _load():
     L.q2d_grouped_tensor_init.argtypes = [TP, I64, I64, I32, I32, ctypes.POINTER(ctypes.c_int64)]
     L.q2d_grouped_quantize.argtypes = [P, I32, I64, I64, I64, I32, P, I32, I32, U64, U64, TP, P]
     L.q2d_grouped_gemm.argtypes = [TP, I32, TP, I32, I32, P, I64, P, I32, I64, I32, P]
+    L.q2d_dequantize.argtypes = [TP, I32, P, I32, I64, P, I64, P]
     L.q2d_status_string.argtypes = [I32]
     L.q2d_status_string.restype = ctypes.c_char_p
     for name in ("q2d_tensor_init", "q2d_quantize", "mxfp8_quantize", "q2d_gemm",
                  "q2d_linear_fwd", "q2d_linear_bwd", "q2d_grouped_tensor_init",
-                 "q2d_grouped_quantize", "q2d_grouped_gemm"):
+                 "q2d_grouped_quantize", "q2d_grouped_gemm", "q2d_quantize_1d", "q2d_dequantize"):
         getattr(L, name).restype = I32
     return L
 
@@ -175,6 +176,24 @@ def mxfp8_quantize(x: torch.Tensor, out: QTensor | None = None) -> QTensor:
     _check(_lib.mxfp8_quantize(x.data_ptr(), _dtype_code(x.dtype), R, C, x.stride(0), x.stride(1),
                                out.ptr(), _stream(x.device)), "mxfp8_quantize")
     return out
+
+
+def q2d_dequantize(q: QTensor, copy: int = 0, out_dtype=torch.float32, exps: bool = False,
+                   out: torch.Tensor | None = None):
+    """Values of one stored copy of ``q`` as an R x C tensor (copy 0: the forward
+    copy codes/scales; 1: the backward copy codes_t/scales_t, mapped back to
+    (r, c)).  With exps=True also returns the int8 scale exponent of every element
+    (-128 for a non-finite block)."""
+    R, C = q.rows, q.cols
+    if out is None:
+        out = torch.empty((R, C), dtype=out_dtype, device=q.device)
+    if out.dim() != 2 or out.stride(1) != 1 or tuple(out.shape) != (R, C):
+        raise Q2DError("output must be a row-major R x C tensor")
+    e = torch.empty((R, C), dtype=torch.int8, device=q.device) if exps else None
+    _check(_lib.q2d_dequantize(q.ptr(), int(copy), out.data_ptr(), _dtype_code(out.dtype), out.stride(0),
+                               e.data_ptr() if e is not None else None, C, _stream(q.device)),
+           "q2d_dequantize")
+    return (out, e) if exps else out
 
 
 def q2d_gemm(A: QTensor, transA: int, B: QTensor, transB: int, out: torch.Tensor | None = None,

@@ -390,6 +390,35 @@ q2d_status q2d_grouped_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B
     return Q2D_OK;
 }
 
+q2d_status q2d_dequantize(const q2d_tensor *t, int copy, void *out, q2d_dtype out_dt, int64_t ldo,
+                          int8_t *exps, int64_t lde, hipStream_t stream)
+{
+    if (!t || !out || (copy != 0 && copy != 1) || !valid_dtype(out_dt)) return Q2D_EINVAL;
+    if (t->fmt != Q2D_FMT_FP4_2D && t->fmt != Q2D_FMT_MXFP8 && t->fmt != Q2D_FMT_FP4_1D) return Q2D_EINVAL;
+    if (t->block != 32 && !(t->block == 64 && t->fmt == Q2D_FMT_FP4_2D)) return Q2D_EUNSUPPORTED;
+    if (t->rows <= 0 || t->cols <= 0 || ldo < t->cols || (exps && lde < t->cols)) return Q2D_EINVAL;
+    const Layout l = layout_of((q2d_fmt)t->fmt, t->rows, t->cols);
+    const uint8_t *codes = copy ? t->codes_t : t->codes;
+    const uint8_t *scales = copy ? t->scales_t : t->scales;
+    const int64_t ldc = copy ? t->ld_codes_t : t->ld_codes, lds = copy ? t->ld_scales_t : t->ld_scales;
+    if (!codes || !check_pair(codes, ldc, copy ? l.ld_codes_t : l.ld_codes, scales, lds,
+                              copy ? l.ld_scales_t : l.ld_scales))
+        return Q2D_EINVAL;
+    const int eb = dtype_bytes(out_dt);
+    DequantArgs a;
+    a.codes = codes; a.ld_codes = ldc;
+    a.scales = scales; a.ld_scales = lds;
+    a.rows = t->rows; a.cols = t->cols;
+    a.fmt = t->fmt == Q2D_FMT_FP4_2D ? 0 : (t->fmt == Q2D_FMT_MXFP8 ? 1 : 2);
+    a.transposed = copy;
+    a.out = out; a.ldo = ldo;
+    a.out_bf16 = out_dt == Q2D_BF16;
+    a.out_vec = aligned(out, 4 * eb) && (ldo % 4) == 0;
+    a.exps = exps; a.lde = lde;
+    if (launch_dequantize(a, stream) != hipSuccess) return Q2D_ELAUNCH;
+    return Q2D_OK;
+}
+
 const char *q2d_status_string(q2d_status s)
 {
     switch (s) {

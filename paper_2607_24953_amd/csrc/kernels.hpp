@@ -68,4 +68,19 @@ struct GroupedArgs {
 
 hipError_t launch_grouped_gemm(const GemmArgs &g, const GroupedArgs &gr, int c_is_bf16, hipStream_t stream);
 
+// Dequantization of one stored copy back to R x C values (row-major out).
+struct DequantArgs {
+    const uint8_t *codes;  int64_t ld_codes;    // the copy read: codes, or codes_t (transposed)
+    const uint8_t *scales; int64_t ld_scales;   // its scales
+    int64_t rows, cols;                         // R x C of the matrix
+    int fmt;                                    // 0 FP4 2D blocks, 1 MXFP8, 2 FP4 1D blocks
+    int transposed;                             // the copy stores element (r, c) in row c
+    void *out; int64_t ldo;                     // elements
+    int out_bf16;
+    int out_vec;                                // out and ldo allow 4-element vector stores
+    int8_t *exps; int64_t lde;                  // optional per-element scale exponents
+};
+
+hipError_t launch_dequantize(const DequantArgs &a, hipStream_t stream);
+
 }  // namespace q2d

@@ -136,6 +136,27 @@ def test_block64_descriptors(q2d):
     assert L.q2d_gemm(ctypes.byref(d), 0, ctypes.byref(f), 0, fake, 0, 64, 0, None) == 1
 
 
+def test_dequantize_error_paths(q2d):
+    L = q2d._lib
+    sizes = (ctypes.c_int64 * 4)()
+    fake = 0x1000
+    d = q2d._Tensor()
+    assert L.q2d_tensor_init(ctypes.byref(d), 0, 64, 96, 32, sizes) == 0
+    assert L.q2d_dequantize(ctypes.byref(d), 0, fake, 0, 96, None, 0, None) == 1     # no buffers
+    d.codes, d.scales = fake, fake
+    assert L.q2d_dequantize(ctypes.byref(d), 1, fake, 0, 96, None, 0, None) == 1     # no codes_t
+    assert L.q2d_dequantize(None, 0, fake, 0, 96, None, 0, None) == 1
+    assert L.q2d_dequantize(ctypes.byref(d), 2, fake, 0, 96, None, 0, None) == 1     # copy
+    assert L.q2d_dequantize(ctypes.byref(d), 0, None, 0, 96, None, 0, None) == 1     # out
+    assert L.q2d_dequantize(ctypes.byref(d), 0, fake, 3, 96, None, 0, None) == 1     # dtype
+    assert L.q2d_dequantize(ctypes.byref(d), 0, fake, 0, 95, None, 0, None) == 1     # ldo < cols
+    assert L.q2d_dequantize(ctypes.byref(d), 0, fake, 0, 96, fake, 90, None) == 1    # lde < cols
+    d.ld_codes = 16
+    assert L.q2d_dequantize(ctypes.byref(d), 0, fake, 0, 96, None, 0, None) == 1     # ld below layout
+    d.block = 16
+    assert L.q2d_dequantize(ctypes.byref(d), 0, fake, 0, 96, None, 0, None) == 2
+
+
 @pytest.mark.parametrize("counts,C", [([0, 1, 31, 33, 127, 130], 96), ([256], 128),
                                       ([5] * 1024, 200), ([0, 0, 0], 32)])
 def test_grouped_layout_holds_oracle_layout(q2d, counts, C):
