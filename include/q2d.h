@@ -55,7 +55,16 @@ typedef enum { Q2D_F32 = 0, Q2D_BF16 = 1 } q2d_dtype;
 
 typedef enum {
     Q2D_RTN = 0,             /* round to nearest, ties to the even E2M1 code (App. E, forward) */
-    Q2D_SR = 1               /* stochastic rounding, Philox4x32-10, 16 bits per element (App. E) */
+    Q2D_SR = 1,              /* stochastic rounding, Philox4x32-10, 16 bits per element (App. E) */
+    /* Flag OR-ed into Q2D_RTN or Q2D_SR for 2D-block FP4 (q2d_quantize,
+     * q2d_grouped_quantize, and the linear-layer calls that use them): the scale
+     * rule that the truncation-free ablation removes (Sec. 4.2, Fig. 5; App. G,
+     * "Truncation-free scaling").  The block exponent becomes
+     * e = floor(log2 M) - 2 (M's leading-bit exponent minus E2M1's largest
+     * exponent, clamped to -127) and magnitudes above 6 * 2^e saturate to 6
+     * before rounding, so a block maximum with mantissa above 1.5 is clipped by
+     * up to 25 %.  Q2D_EUNSUPPORTED for the 1D quantizer. */
+    Q2D_FLOOR_SCALE = 0x10
 } q2d_round;
 
 typedef enum {

@@ -59,6 +59,8 @@ def lib():
         L.or_sr_bits.restype = ctypes.c_uint32
         L.or_fp4_scale_exponent.argtypes = [ctypes.c_double]
         L.or_fp4_scale_exponent.restype = I32
+        L.or_fp4_floor_exponent.argtypes = [ctypes.c_double]
+        L.or_fp4_floor_exponent.restype = I32
         L.or_fp8_scale_exponent.argtypes = [ctypes.c_double]
         L.or_fp8_scale_exponent.restype = I32
         L.or_fp4_code.argtypes = [ctypes.c_double, I32, I32, ctypes.c_uint32]
@@ -98,6 +100,11 @@ def sr_bits(idx: int, seed: int, offset: int) -> int:
 
 def fp4_scale_exponent(M: float) -> int:
     return int(lib().or_fp4_scale_exponent(float(M)))
+
+
+def fp4_floor_exponent(M: float) -> int:
+    """Scale exponent of the truncation-free ablation: floor(log2 M) - 2, clamped to -127."""
+    return int(lib().or_fp4_floor_exponent(float(M)))
 
 
 def fp8_scale_exponent(M: float) -> int:
@@ -244,6 +251,15 @@ def to_float64(x) -> np.ndarray:
 
 # ------------------------------------------------------------------ quantizers
 
+def _mode_bits(mode: str) -> int:
+    """Rounding and scale rule of the 2D quantizer: bit 0 stochastic rounding, bit 1
+    the floor scale rule of the truncation-free ablation ("rtn-floor", "sr-floor")."""
+    bits = {"rtn": 0, "sr": 1, "rtn-floor": 2, "sr-floor": 3}
+    if mode not in bits:
+        raise ValueError("unknown rounding mode " + repr(mode))
+    return bits[mode]
+
+
 def quantize_fp4_2d(x, mode: str = "rtn", seed: int = 0, offset: int = 0,
                     threads: int = 0, index_base: int = 0, block: int = BLOCK) -> dict:
     """2D-block FP4 quantization of a 2-D CPU tensor into both packed layouts.
@@ -263,7 +279,7 @@ def quantize_fp4_2d(x, mode: str = "rtn", seed: int = 0, offset: int = 0,
         nr, nc = -(-R // block), -(-C // block)
         sc_buf, sct_buf = np.zeros((nr, nc), np.uint8), np.zeros((nc, nr), np.uint8)
     lib().or_quantize_fp4_2d(ptr, dt, R, C, sr, sc, int(index_base), int(block),
-                             1 if mode == "sr" else 0,
+                             _mode_bits(mode),
                              int(seed), int(offset),
                              out["codes"].ctypes.data, lay["codes"][1],
                              out["codes_t"].ctypes.data, lay["codes_t"][1],
@@ -298,7 +314,7 @@ def quantize_fp4_grouped(x, offsets, mode: str = "rtn", seed: int = 0, offset: i
         base = ptr + int(off[e]) * sr * esize
         pe = int(p[e])
         lib().or_quantize_fp4_2d(
-            base, dt, n, C, sr, sc, int(off[e]) * sr, BLOCK, 1 if mode == "sr" else 0,
+            base, dt, n, C, sr, sc, int(off[e]) * sr, BLOCK, _mode_bits(mode),
             int(seed), int(offset),
             out["codes"].ctypes.data + pe * lay["codes"][1], lay["codes"][1],
             out["codes_t"].ctypes.data + pe // 2, lay["codes_t"][1],

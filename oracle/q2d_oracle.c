@@ -97,6 +97,21 @@ static int tf_exponent(double M, double qmax)
 }
 
 int or_fp4_scale_exponent(double M) { return tf_exponent(M, 6.0); }
+
+/*
+ * The scale rule that the truncation-free ablation goes back to (Sec. 4.2, the
+ * ablation figure; App. G, "Truncation-free scaling"): the shared exponent of
+ * the OCP microscaling formats, floor(log2 M) minus the largest E2M1 exponent
+ * (2, as 6 = 1.5 * 2^2): the largest integer e with 4 * 2^e <= M, searched
+ * upward from the clamp -127.  Elements above 6 * 2^e then saturate to +-6
+ * (or_fp4_code never returns a magnitude above index 7).
+ */
+int or_fp4_floor_exponent(double M)
+{
+    int e = -127;
+    while (e < 127 && 4.0 * ldexp(1.0, e + 1) <= M) ++e;
+    return e;
+}
 int or_fp8_scale_exponent(double M) { return tf_exponent(M, 448.0); }
 
 /* ---------------------------------------------------------------- FP4 element */
@@ -176,7 +191,8 @@ static void put_nibble(uint8_t *row, int64_t pos, unsigned code)
  * Quantize the R x C matrix x[r*sr + c*sc] (sr, sc in elements) into 2D-block
  * FP4.  idx0 is added to every storage index before it keys the random stream
  * (0 for a whole tensor; the segment's first storage index for a grouped one).
- * mode 0: round to nearest; 1: stochastic.
+ * mode bit 0: stochastic rounding (else round to nearest); bit 1: the floor
+ * scale rule of the truncation-free ablation (else the truncation-free rule).
  */
 void or_quantize_fp4_2d(const void *x, int dtype, int64_t R, int64_t C, int64_t sr, int64_t sc,
                         int64_t idx0, int b, int mode, uint64_t seed, uint64_t offset,
@@ -201,7 +217,7 @@ void or_quantize_fp4_2d(const void *x, int dtype, int64_t R, int64_t C, int64_t 
                     if (!isfinite(v)) finite = 0;
                     else if (fabs(v) > M) M = fabs(v);
                 }
-            int e = or_fp4_scale_exponent(M);
+            int e = (mode & 2) ? or_fp4_floor_exponent(M) : or_fp4_scale_exponent(M);
             uint8_t sbyte = finite ? (uint8_t)(e + 127) : 0xFF;
             if (scales) scales[I * lds + J] = sbyte;
             if (scales_t) scales_t[J * ldst + I] = sbyte;
@@ -210,8 +226,8 @@ void or_quantize_fp4_2d(const void *x, int dtype, int64_t R, int64_t C, int64_t 
                     unsigned code = 0;
                     if (finite) {
                         int64_t idx = r * sr + c * sc;
-                        uint32_t r16 = mode ? or_sr_bits(idx0 + idx, seed, offset) : 0;
-                        code = or_fp4_code(load(x, dtype, idx), e, mode, r16);
+                        uint32_t r16 = (mode & 1) ? or_sr_bits(idx0 + idx, seed, offset) : 0;
+                        code = or_fp4_code(load(x, dtype, idx), e, mode & 1, r16);
                     }
                     if (codes) put_nibble(codes + r * ldc, c, code);
                     if (codes_t) put_nibble(codes_t + c * ldt, r, code);

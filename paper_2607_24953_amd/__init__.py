@@ -14,7 +14,7 @@ import os
 import torch
 
 __all__ = [
-    "Q2DError", "QTensor", "RTN", "SR", "FP4_2D", "MXFP8", "FP4_1D", "lib_path",
+    "Q2DError", "QTensor", "RTN", "SR", "FLOOR_SCALE", "FP4_2D", "MXFP8", "FP4_1D", "lib_path",
     "q2d_tensor_init", "q2d_quantize", "q2d_quantize_1d", "mxfp8_quantize", "q2d_gemm",
     "q2d_linear_fwd", "q2d_linear_bwd", "q2d_grouped_tensor_init", "q2d_grouped_quantize",
     "q2d_grouped_gemm", "q2d_dequantize", "q2d_status_string",
@@ -26,7 +26,10 @@ lib_path = os.path.join(_HERE, "libq2d.so")
 RTN, SR = 0, 1
 FP4_2D, MXFP8, FP4_1D = 0, 1, 2
 _F32, _BF16 = 0, 1
-_ROUND = {"rtn": RTN, "sr": SR, RTN: RTN, SR: SR}
+FLOOR_SCALE = 0x10        # scale rule of the truncation-free ablation (2D FP4 only)
+_ROUND = {"rtn": RTN, "sr": SR, RTN: RTN, SR: SR,
+          "rtn-floor": RTN | FLOOR_SCALE, "sr-floor": SR | FLOOR_SCALE,
+          RTN | FLOOR_SCALE: RTN | FLOOR_SCALE, SR | FLOOR_SCALE: SR | FLOOR_SCALE}
 
 
 class Q2DError(RuntimeError):

@@ -102,6 +102,7 @@ QuantArgs make_quant_args(const void *x, int64_t R, int64_t C, int64_t sr, int64
     a.nseg = 0;
     a.store_rows = a.rows;
     a.block = 32;
+    a.floor_scale = 0;
     return a;
 }
 
@@ -151,14 +152,16 @@ q2d_status q2d_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols,
 {
     q2d_status s = check_input(x, dt, rows, cols, stride_r, stride_c);
     if (s != Q2D_OK) return s;
-    if (mode != Q2D_RTN && mode != Q2D_SR) return Q2D_EINVAL;
+    const int rmode = (int)mode & ~Q2D_FLOOR_SCALE;
+    if (rmode != Q2D_RTN && rmode != Q2D_SR) return Q2D_EINVAL;
     if (block != 32 && block != 64) return Q2D_EUNSUPPORTED;
     s = check_tensor(out, Q2D_FMT_FP4_2D, rows, cols);
     if (s != Q2D_OK) return s;
     if (out->block != block) return Q2D_EINVAL;
     QuantArgs a = make_quant_args(x, rows, cols, stride_r, stride_c, seed, offset, out);
     a.block = block;
-    if (launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, false, stream) != hipSuccess) return Q2D_ELAUNCH;
+    a.floor_scale = ((int)mode & Q2D_FLOOR_SCALE) != 0;
+    if (launch_fp4_quantize(a, dtype_bytes(dt), rmode == Q2D_SR, false, stream) != hipSuccess) return Q2D_ELAUNCH;
     return Q2D_OK;
 }
 
@@ -168,6 +171,7 @@ q2d_status q2d_quantize_1d(const void *x, q2d_dtype dt, int64_t rows, int64_t co
 {
     q2d_status s = check_input(x, dt, rows, cols, stride_r, stride_c);
     if (s != Q2D_OK) return s;
+    if ((int)mode & Q2D_FLOOR_SCALE) return Q2D_EUNSUPPORTED;     // the ablation rule is 2D only
     if (mode != Q2D_RTN && mode != Q2D_SR) return Q2D_EINVAL;
     if (block != 32) return Q2D_EUNSUPPORTED;
     s = check_tensor(out, Q2D_FMT_FP4_1D, rows, cols);
@@ -302,7 +306,8 @@ q2d_status q2d_grouped_quantize(const void *x, q2d_dtype dt, int64_t rows, int64
     q2d_status s = check_input(x, dt, rows > 0 ? rows : 1, cols, stride_r, 1);
     if (s != Q2D_OK) return s;
     if (rows <= 0 || stride_r < cols) return Q2D_EINVAL;
-    if (mode != Q2D_RTN && mode != Q2D_SR) return Q2D_EINVAL;
+    const int rmode = (int)mode & ~Q2D_FLOOR_SCALE;
+    if (rmode != Q2D_RTN && rmode != Q2D_SR) return Q2D_EINVAL;
     if (block != 32) return Q2D_EUNSUPPORTED;
     const int64_t cap = grouped_capacity(rows, nseg);
     s = check_tensor(out, Q2D_FMT_FP4_2D, cap, cols);
@@ -312,7 +317,8 @@ q2d_status q2d_grouped_quantize(const void *x, q2d_dtype dt, int64_t rows, int64
     a.rows_pad = cap;               // grid bound over padded rows
     a.seg_offsets = seg_offsets;
     a.nseg = nseg;
-    if (launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, false, stream) != hipSuccess) return Q2D_ELAUNCH;
+    a.floor_scale = ((int)mode & Q2D_FLOOR_SCALE) != 0;
+    if (launch_fp4_quantize(a, dtype_bytes(dt), rmode == Q2D_SR, false, stream) != hipSuccess) return Q2D_ELAUNCH;
     return Q2D_OK;
 }
 

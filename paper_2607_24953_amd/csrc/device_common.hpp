@@ -56,6 +56,16 @@ __device__ __forceinline__ int fp4_block_exponent(uint32_t amax_bits)
     return e < -127 ? -127 : e;
 }
 
+// Scale rule of the truncation-free ablation (the shared-exponent rule of the
+// OCP microscaling formats): e = floor(log2 M) - 2, the exponent of M's leading
+// bit minus E2M1's largest exponent (6 = 1.5 * 2^2), clamped to -127.  Block
+// maxima with a mantissa above 1.5 then exceed 6 * 2^e and saturate to +-6.
+__device__ __forceinline__ int fp4_floor_exponent(uint32_t amax_bits)
+{
+    const int e = (int)(amax_bits >> 23) - 129;
+    return e < -127 ? -127 : e;
+}
+
 // Same rule for E4M3 (largest magnitude 448 = 1.75 * 2^8): e = p - 8, plus one
 // when f > 1.75.
 __device__ __forceinline__ int fp8_block_exponent(uint32_t amax_bits)

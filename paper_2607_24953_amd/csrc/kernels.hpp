@@ -29,6 +29,7 @@ struct QuantArgs {
     int32_t nseg;
     int64_t store_rows;            // rows of codes / scales written (>= rows; padded rows get zeros)
     int32_t block;                 // 2D block edge: 32, or 64 (its scale written to the four 32-entries)
+    int32_t floor_scale;           // 2D FP4: floor scale rule with saturation instead of the truncation-free one
 };
 
 // 2D blocks, or 1D blocks (oned: 1 x 32 rowwise copy, 32 x 1 colwise copy)

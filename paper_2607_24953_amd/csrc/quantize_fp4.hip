@@ -287,8 +287,27 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
         am = max(am, am64[wr ^ 1][wc * 2 + (cc >> 3)]);
     }
     const bool finite = am < 0x7F800000u;
-    const int e = fp4_block_exponent(am);
+    const bool floor_rule = !ONED && a.floor_scale;
+    const int e = floor_rule ? fp4_floor_exponent(am) : fp4_block_exponent(am);
     const float scale = bits_f((uint32_t)(127 + e) << 23);       // 2^e
+    if (floor_rule && finite) {
+        // saturate magnitudes above 6 * 2^e (exact in bf16: 1.5 * 2^(e+2))
+        const uint32_t lim = ((uint32_t)(e + 129) << 23) | 0x400000u;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int k = 0; k < NV; ++k) {
+                if (PK) {
+                    const uint32_t l16 = lim >> 16;
+                    uint32_t lo = v[i][k] & 0xFFFFu, hi = v[i][k] >> 16;
+                    if ((lo & 0x7FFFu) > l16) lo = (lo & 0x8000u) | l16;
+                    if ((hi & 0x7FFFu) > l16) hi = (hi & 0x8000u) | l16;
+                    v[i][k] = lo | (hi << 16);
+                } else if ((v[i][k] & 0x7FFFFFFFu) > lim) {
+                    v[i][k] = (v[i][k] & 0x80000000u) | lim;
+                }
+            }
+    }
     // scale of row i / column j of the sub-block (the block scale for 2D)
     auto rscale = [&](int i) -> float {
         return ONED ? bits_f((uint32_t)(127 + fp4_block_exponent(rm[i])) << 23) : scale;

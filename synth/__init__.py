@@ -28,7 +28,7 @@ import torch
 
 __all__ = [
     "normal", "add_outlier_channels", "moe_counts", "segment_offsets",
-    "Workload", "tiny", "dense_1b", "dense_7b", "dense_7b_1d", "dense_7b_b64", "moe_30b", "mixed_7b", "WORKLOADS",
+    "Workload", "student_t", "regression_task", "tiny", "dense_1b", "dense_7b", "dense_7b_1d", "dense_7b_b64", "moe_30b", "mixed_7b", "WORKLOADS",
 ]
 
 
@@ -64,6 +64,30 @@ def add_outlier_channels(x: torch.Tensor, seed: int, frac: float = 0.01,
     t = z / torch.sqrt(chi2 / nu)
     x[:, idx] = (scale * t).to(x.dtype)
     return x
+
+
+def student_t(shape, nu: int, seed: int, device="cpu") -> torch.Tensor:
+    """Float32 Student-t(nu) samples: z / sqrt(chi2_nu / nu) from seeded normals."""
+    g = _gen(seed, device)
+    z = torch.randn(tuple(shape), generator=g, device=device, dtype=torch.float32)
+    chi2 = torch.zeros(tuple(shape), device=device, dtype=torch.float32)
+    for _ in range(nu):
+        w = torch.randn(tuple(shape), generator=g, device=device, dtype=torch.float32)
+        chi2.add_(w * w)
+    return z / torch.sqrt(chi2 / nu)
+
+
+def regression_task(tokens: int, k_in: int, n_out: int, noise: float, nu: int, seed: int, device="cpu"):
+    """Teacher-student linear regression: X ~ N(0, 1) [tokens, k_in], teacher
+    W* ~ N(0, 1/k_in) [n_out, k_in], targets X W*^T + noise * Student-t(nu)
+    (heavy-tailed residuals, so the output gradients of a 32 x 32 block span a
+    wide range).  Returns float32 (X, W*, Y)."""
+    X = normal((tokens, k_in), 1.0, seed, torch.float32, device)
+    W = normal((n_out, k_in), 1.0 / float(k_in) ** 0.5, seed + 1, torch.float32, device)
+    Y = X @ W.t()
+    if noise:
+        Y = Y + noise * student_t((tokens, n_out), nu, seed + 2, device)
+    return X, W, Y
 
 
 def moe_counts(tokens: int = 16384, experts: int = 128, topk: int = 8,

@@ -70,6 +70,8 @@ def test_error_paths(q2d):
     assert L.q2d_quantize(fake, 1, 65, 64, 64, 1, 32, 0, 0, 0, ctypes.byref(d), None) == 1
     assert L.q2d_quantize(fake, 1, 64, 64, 0, 1, 32, 0, 0, 0, ctypes.byref(d), None) == 1
     assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 32, 9, 0, 0, ctypes.byref(d), None) == 1
+    assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 32, 0x12, 0, 0, ctypes.byref(d), None) == 1  # flag + bad mode
+    assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 32, 0x30, 0, 0, ctypes.byref(d), None) == 1  # unknown flag
     assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 16, 0, 0, 0, ctypes.byref(d), None) == 2
     assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 64, 0, 0, 0, ctypes.byref(d), None) == 1   # != out->block
     assert L.q2d_quantize(fake + 1, 1, 64, 64, 64, 1, 32, 0, 0, 0, ctypes.byref(d), None) == 1
@@ -103,6 +105,7 @@ def test_error_paths(q2d):
     assert L.q2d_quantize(fake, 1, 64, 64, 64, 1, 32, 0, 0, 0, ctypes.byref(h), None) == 1      # 1D descriptor
     assert L.q2d_quantize_1d(fake, 1, 64, 64, 64, 1, 64, 0, 0, 0, ctypes.byref(h), None) == 2
     assert L.q2d_quantize_1d(fake, 1, 64, 64, 64, 1, 32, 9, 0, 0, ctypes.byref(h), None) == 1
+    assert L.q2d_quantize_1d(fake, 1, 64, 64, 64, 1, 32, 0x10, 0, 0, ctypes.byref(h), None) == 2  # floor rule: 2D only
     assert L.q2d_gemm(ctypes.byref(h), 0, ctypes.byref(f), 0, fake, 0, 64, 0, None) == 1
     assert L.q2d_gemm(ctypes.byref(f), 0, ctypes.byref(h), 0, fake, 0, 64, 0, None) == 1
     assert q2d.q2d_status_string(2) == "unsupported configuration"
