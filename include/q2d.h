@@ -216,6 +216,29 @@ q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int tr
                     void *C, q2d_dtype c_dt, int64_t ldc, int accumulate, hipStream_t stream);
 
 /*
+ * GEMM with its result quantized in the epilogue: the float32 result C =
+ * op(A) op(B)^T (as q2d_gemm computes it, never written out) goes straight
+ * into 2D-block FP4 with round to nearest -- the truncation-free scale of each
+ * 32x32 block and the E2M1 codec of q2d_quantize -- in both orientations.  The
+ * output of one linear layer then enters the next GEMM without a bfloat16
+ * round trip through memory (App. C: Y and dX are operands of further GEMMs).
+ * Each 32x32 block of C is one 32x32 MFMA tile, so its maximum is found in the
+ * tile's registers.
+ *
+ * A, B, transA, transB as for q2d_gemm (FP4_2D and FP4_1D operands).
+ * mode     Q2D_RTN (Q2D_SR: Q2D_EUNSUPPORTED; stochastic rounding of a GEMM
+ *          output is left to q2d_quantize).
+ * out      descriptor from q2d_tensor_init(FP4_2D, M, N, 32) with all four
+ *          buffers attached; written as q2d_quantize writes it (padding
+ *          included).  A block holding a NaN or an infinity gets scale 0xFF
+ *          and zero codes.
+ * Q2D_EUNSUPPORTED for MXFP8 operands, block 64 output, or operands beyond
+ * 4 GiB.  Stream-ordered.
+ */
+q2d_status q2d_gemm_quantized(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, q2d_round mode,
+                              q2d_tensor *out, hipStream_t stream);
+
+/*
  * Forward pass of a quantized linear layer Y = X W^T (Sec. 3; App. C):
  * quantizes X [T][K] and W [N][K] (row-major, dtype dt) into qX and qW (both
  * orientations, kept for the backward pass) and runs the forward GEMM into

@@ -456,6 +456,17 @@ def gemm(a: np.ndarray, b: np.ndarray) -> np.ndarray:
     return np.asarray(a, dtype=np.float64) @ np.asarray(b, dtype=np.float64).T
 
 
+def gemm_quantized(a: np.ndarray, b: np.ndarray) -> dict:
+    """A GEMM whose result is quantized (App. C: a layer's output is the next
+    GEMM's operand): C = A B^T in float64, rounded once to float32 (the
+    precision the result has before it is quantized), then 2D-block FP4 with
+    round to nearest."""
+    c = gemm(a, b)
+    with np.errstate(over="ignore"):
+        c32 = c.astype(np.float32)
+    return quantize_fp4_2d(np.ascontiguousarray(c32), "rtn")
+
+
 def linear(qx: dict, qw: dict, qdy: dict, fmt: str = "fp4", fmt_x: str | None = None) -> dict:
     """The three GEMMs of a linear layer on quantized operands (App. C):
     Y = X W^T, dX = dY W, dW = dY^T X, each operand quantized once.  fmt_x

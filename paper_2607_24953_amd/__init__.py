@@ -17,7 +17,7 @@ __all__ = [
     "Q2DError", "QTensor", "RTN", "SR", "FLOOR_SCALE", "FP4_2D", "MXFP8", "FP4_1D", "lib_path",
     "q2d_tensor_init", "q2d_quantize", "q2d_quantize_1d", "mxfp8_quantize", "q2d_gemm",
     "q2d_linear_fwd", "q2d_linear_bwd", "q2d_grouped_tensor_init", "q2d_grouped_quantize",
-    "q2d_grouped_gemm", "q2d_dequantize", "q2d_status_string",
+    "q2d_grouped_gemm", "q2d_dequantize", "q2d_gemm_quantized", "q2d_status_string",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -62,11 +62,13 @@ def _load():
     L.q2d_grouped_quantize.argtypes = [P, I32, I64, I64, I64, I32, P, I32, I32, U64, U64, TP, P]
     L.q2d_grouped_gemm.argtypes = [TP, I32, TP, I32, I32, P, I64, P, I32, I64, I32, P]
     L.q2d_dequantize.argtypes = [TP, I32, P, I32, I64, P, I64, P]
+    L.q2d_gemm_quantized.argtypes = [TP, I32, TP, I32, I32, TP, P]
     L.q2d_status_string.argtypes = [I32]
     L.q2d_status_string.restype = ctypes.c_char_p
     for name in ("q2d_tensor_init", "q2d_quantize", "mxfp8_quantize", "q2d_gemm",
                  "q2d_linear_fwd", "q2d_linear_bwd", "q2d_grouped_tensor_init",
-                 "q2d_grouped_quantize", "q2d_grouped_gemm", "q2d_quantize_1d", "q2d_dequantize"):
+                 "q2d_grouped_quantize", "q2d_grouped_gemm", "q2d_quantize_1d", "q2d_dequantize",
+                 "q2d_gemm_quantized"):
         getattr(L, name).restype = I32
     return L
 
@@ -211,6 +213,19 @@ def q2d_gemm(A: QTensor, transA: int, B: QTensor, transB: int, out: torch.Tensor
     _check(_lib.q2d_gemm(A.ptr(), int(transA), B.ptr(), int(transB), out.data_ptr(),
                          _dtype_code(out.dtype), out.stride(0), int(bool(accumulate)),
                          _stream(A.device)), "q2d_gemm")
+    return out
+
+
+def q2d_gemm_quantized(A: QTensor, transA: int, B: QTensor, transB: int, mode="rtn",
+                       out: QTensor | None = None) -> QTensor:
+    """op(A) op(B)^T quantized to 2D-block FP4 (round to nearest) in the GEMM's
+    epilogue; returns the quantized result with both orientations."""
+    M = A.cols if transA else A.rows
+    N = B.cols if transB else B.rows
+    if out is None:
+        out = QTensor(FP4_2D, M, N, A.device)
+    _check(_lib.q2d_gemm_quantized(A.ptr(), int(transA), B.ptr(), int(transB), _ROUND[mode], out.ptr(),
+                                   _stream(A.device)), "q2d_gemm_quantized")
     return out
 
 

@@ -207,12 +207,12 @@ q2d_status mxfp8_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t col
     return Q2D_OK;
 }
 
-q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, void *C,
-                    q2d_dtype c_dt, int64_t ldc, int accumulate, hipStream_t stream)
+// Operands of a GEMM C = op(A) op(B)^T into g (codes, scales, M, N, padded K,
+// 1D flags); fp4 tells the FP4 pairing from the MXFP8 one.
+static q2d_status gemm_operands(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, GemmArgs &g, bool &fp4)
 {
-    if (!A || !B || !C || !valid_dtype(c_dt)) return Q2D_EINVAL;
+    if (!A || !B) return Q2D_EINVAL;
     if ((transA != 0 && transA != 1) || (transB != 0 && transB != 1)) return Q2D_EINVAL;
-    if (accumulate != 0 && accumulate != 1) return Q2D_EINVAL;
     // FP4 operands may mix 2D and 1D blocks (activations); MXFP8 pairs with MXFP8
     const bool fp4a = A->fmt == Q2D_FMT_FP4_2D || A->fmt == Q2D_FMT_FP4_1D;
     const bool fp4b = B->fmt == Q2D_FMT_FP4_2D || B->fmt == Q2D_FMT_FP4_1D;
@@ -225,10 +225,9 @@ q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int tr
     if (A->rows <= 0 || A->cols <= 0 || B->rows <= 0 || B->cols <= 0) return Q2D_EINVAL;
     const int64_t M = transA ? A->cols : A->rows, Ka = transA ? A->rows : A->cols;
     const int64_t N = transB ? B->cols : B->rows, Kb = transB ? B->rows : B->cols;
-    if (Ka != Kb || ldc < N) return Q2D_EINVAL;
-    if (!aligned(C, (uintptr_t)dtype_bytes(c_dt))) return Q2D_EINVAL;
+    if (Ka != Kb) return Q2D_EINVAL;
     const Layout la = layout_of((q2d_fmt)A->fmt, A->rows, A->cols), lb = layout_of((q2d_fmt)B->fmt, B->rows, B->cols);
-    GemmArgs g;
+    g = GemmArgs{};
     g.a1d = A->fmt == Q2D_FMT_FP4_1D;
     g.b1d = B->fmt == Q2D_FMT_FP4_1D;
     if (!transA) {
@@ -251,11 +250,51 @@ q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int tr
             return Q2D_EINVAL;
         g.b = B->codes_t; g.ldb = B->ld_codes_t; g.sb = B->scales_t; g.ldsb = B->ld_scales_t;
     }
-    g.c = C; g.ldc = ldc;
     g.M = M; g.N = N; g.K = rup(Ka, kPadK);
+    fp4 = fp4a;
+    return Q2D_OK;
+}
+
+q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, void *C,
+                    q2d_dtype c_dt, int64_t ldc, int accumulate, hipStream_t stream)
+{
+    if (!A || !B || !C || !valid_dtype(c_dt)) return Q2D_EINVAL;
+    if (accumulate != 0 && accumulate != 1) return Q2D_EINVAL;
+    GemmArgs g;
+    bool fp4 = false;
+    const q2d_status s = gemm_operands(A, transA, B, transB, g, fp4);
+    if (s != Q2D_OK) return s;
+    if (ldc < g.N) return Q2D_EINVAL;
+    if (!aligned(C, (uintptr_t)dtype_bytes(c_dt))) return Q2D_EINVAL;
+    g.c = C; g.ldc = ldc;
     g.accumulate = accumulate;
-    if (launch_gemm(g, fp4a ? kFmtFp4Block2D : kFmtMxfp8, c_dt == Q2D_BF16, stream) != hipSuccess)
+    if (launch_gemm(g, fp4 ? kFmtFp4Block2D : kFmtMxfp8, c_dt == Q2D_BF16, stream) != hipSuccess)
         return Q2D_ELAUNCH;
+    return Q2D_OK;
+}
+
+q2d_status q2d_gemm_quantized(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, q2d_round mode,
+                              q2d_tensor *out, hipStream_t stream)
+{
+    if (!A || !B || !out) return Q2D_EINVAL;
+    if (mode != Q2D_RTN) return mode == Q2D_SR ? Q2D_EUNSUPPORTED : Q2D_EINVAL;
+    GemmArgs g;
+    bool fp4 = false;
+    q2d_status s = gemm_operands(A, transA, B, transB, g, fp4);
+    if (s != Q2D_OK) return s;
+    if (!fp4) return Q2D_EUNSUPPORTED;
+    s = check_tensor(out, Q2D_FMT_FP4_2D, g.M, g.N);
+    if (s != Q2D_OK) return s;
+    if (out->block != 32) return Q2D_EUNSUPPORTED;
+    if (!out->codes || !out->codes_t) return Q2D_EINVAL;
+    // the epilogue stores 8-byte runs of codes_t
+    if (!aligned(out->codes_t, 16) || (out->ld_codes_t % 16) != 0) return Q2D_EINVAL;
+    g.qc = out->codes; g.ldqc = out->ld_codes;
+    g.qct = out->codes_t; g.ldqct = out->ld_codes_t;
+    g.qs = out->scales; g.ldqs = out->ld_scales;
+    g.qst = out->scales_t; g.ldqst = out->ld_scales_t;
+    if (g.M * g.lda > (int64_t(1) << 32) || g.N * g.ldb > (int64_t(1) << 32)) return Q2D_EUNSUPPORTED;
+    if (launch_gemm_quantized(g, stream) != hipSuccess) return Q2D_ELAUNCH;
     return Q2D_OK;
 }
 
@@ -335,7 +374,7 @@ q2d_status q2d_grouped_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B
     if (!aligned(C, (uintptr_t)dtype_bytes(c_dt))) return Q2D_EINVAL;
     const int64_t cap = grouped_capacity(total_rows, nseg);
     const Layout la = layout_of(Q2D_FMT_FP4_2D, A->rows, A->cols), lb = layout_of(Q2D_FMT_FP4_2D, B->rows, B->cols);
-    GemmArgs g;
+    GemmArgs g = {};
     g.a1d = g.b1d = 0;
     GroupedArgs gr;
     gr.seg_offsets = seg_offsets;

@@ -18,6 +18,7 @@
 // Workgroups are remapped so that each XCD (one L2) walks a contiguous band of
 // output tiles, grouped by 8 row tiles for operand reuse.
 #include <atomic>
+#include <type_traits>
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -456,12 +457,158 @@ __device__ __forceinline__ void store_block(v16f (&acc)[4][4], uint8_t *cbase, u
         }
 }
 
+// Quantize a wave's 128 x 128 accumulator block into 2D-block FP4 with round to
+// nearest (the quantizer's scale rule and codec, applied to the float32
+// result): each 32 x 32 MFMA tile is exactly one block.
+//   1. block maxima: each lane's maximum over the 16 values it holds of every
+//      tile, then the 16 maxima reduced across the wave together (quad and row
+//      permutes, then two lane exchanges), so the reductions overlap; with
+//      CHECK, values outside rows_left x cols_left count as 0 (padding gets
+//      zero codes, an all-zero block the byte 0x00);
+//   2. per 32-row strip i, per tile j:
+//      codes_t: a lane holds one column's rows 8q + 4h + 0..3 (h = lane / 32),
+//               two bytes per q; the halves h swap one word so that each lane
+//               stores 8 consecutive bytes of its column's 16-byte run;
+//      codes:   neighbouring columns meet through a quad permute; the even lane
+//               packs rows q = 0, 1 and the odd lane rows q = 2, 3, one byte per
+//               row, into the wave's LDS strip (32 rows x 64 bytes);
+//      scales:  one byte per tile in each grid;
+//      then the strip leaves as 16-byte row segments.
+// Only the written extent of the layout is touched: codes rows < M, bytes below
+// roundup(N, 128) / 2; codes_t rows < N, bytes below roundup(M, 128) / 2.
+constexpr int kQPitch = 80;                     // LDS strip row pitch (64 bytes + pad)
+constexpr int kQStrip = 32 * kQPitch;           // per wave
+
+template <bool CHECK>
+__device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &g, uint8_t *strip, int r0, int c0,
+                                             int rows_left, int cols_left)
+{
+    const int lane = threadIdx.x & 63;
+    const int col = lane & 31, h = lane >> 5, odd = lane & 1;
+    const int padm = (int)((g.M + 127) / 128 * 128), padn = (int)((g.N + 127) / 128 * 128);
+    int dummy = 0;
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+s"(dummy));   // the last MFMA results settle
+    auto value = [&](int i, int j, int r) __attribute__((always_inline)) -> float {
+        float v;
+        asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v) : "a"(acc[i][j][r]));
+        if (CHECK) {
+            const int rr = 32 * i + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (rr >= rows_left || 32 * j + col >= cols_left) v = 0.0f;
+        }
+        return v;
+    };
+    uint32_t am[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            uint32_t m = 0;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) m = max(m, f_bits(value(i, j, r)) & 0x7FFFFFFFu);
+            am[i][j] = m;
+        }
+    // quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror
+    auto perm_max = [&](auto ctrl) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                am[i][j] = max(am[i][j], (uint32_t)__builtin_amdgcn_update_dpp((int)am[i][j], (int)am[i][j],
+                                                                               decltype(ctrl)::value, 0xF, 0xF, false));
+    };
+    perm_max(std::integral_constant<int, 0xB1>{});
+    perm_max(std::integral_constant<int, 0x4E>{});
+    perm_max(std::integral_constant<int, 0x141>{});
+    perm_max(std::integral_constant<int, 0x140>{});
+#pragma unroll
+    for (int m = 16; m < 64; m <<= 1)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) am[i][j] = max(am[i][j], (uint32_t)__shfl_xor((int)am[i][j], m));
+
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int tr = r0 + 32 * i;                     // strip origin row in C
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int tc = c0 + 32 * j;                 // tile origin column
+            const bool finite = am[i][j] < 0x7F800000u;
+            const int e = fp4_block_exponent(am[i][j]);
+            const float scale = bits_f((uint32_t)(127 + e) << 23);
+            float v[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) v[r] = value(i, j, r);
+            // column-packed: word q/2 byte 2 (q % 2) + k holds rows (8q + 4h + 2k, +1)
+            uint32_t w0 = 0, w1 = 0;
+            w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[0], v[1], scale, 0);
+            w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[2], v[3], scale, 1);
+            w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[4], v[5], scale, 2);
+            w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[6], v[7], scale, 3);
+            w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[8], v[9], scale, 0);
+            w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[10], v[11], scale, 1);
+            w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[12], v[13], scale, 2);
+            w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[14], v[15], scale, 3);
+            if (!finite) w0 = w1 = 0;
+            // half 0 stores bytes 0..7 of the run (q = 0, 1 of both halves), half 1
+            // bytes 8..15 (q = 2, 3)
+            const uint32_t mine = h ? w1 : w0;
+            const uint32_t other = (uint32_t)__shfl_xor((int)(h ? w0 : w1), 32);
+            const uint32_t first = h ? other : mine, second = h ? mine : other;
+            const uint2 run = make_uint2((first & 0xFFFFu) | (second << 16), (first >> 16) | (second & 0xFFFF0000u));
+            if (tc + col < g.N && tr < padm)
+                *reinterpret_cast<uint2 *>(g.qct + (int64_t)(tc + col) * g.ldqct + tr / 2 + 8 * h) = run;
+            // row-packed: the neighbouring column's values through a quad permute
+            uint32_t rowb[2] = {0, 0};
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const float send = odd ? v[k] : v[8 + k];      // what the neighbour packs
+                const float nb = __int_as_float(__builtin_amdgcn_update_dpp(
+                    __float_as_int(send), __float_as_int(send), 0xB1, 0xF, 0xF, false));
+                const float own = odd ? v[8 + k] : v[k];
+                const float lo = odd ? nb : own, hi = odd ? own : nb;
+                uint32_t &w = rowb[k >> 2];
+                switch (k & 3) {
+                case 0: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 0); break;
+                case 1: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 1); break;
+                case 2: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 2); break;
+                default: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 3); break;
+                }
+            }
+            if (!finite) rowb[0] = rowb[1] = 0;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int rk = odd ? 8 + k : k;
+                const int rl = 8 * (rk >> 2) + 4 * h + (rk & 3);
+                strip[rl * kQPitch + 16 * j + (col >> 1)] = (uint8_t)(rowb[k >> 2] >> (8 * (k & 3)));
+            }
+            if (lane == 0) {
+                const uint8_t sbyte = finite ? (uint8_t)(e + 127) : (uint8_t)0xFF;
+                if (tr < g.M && tc < padn) g.qs[(int64_t)(tr / 32) * g.ldqs + tc / 32] = sbyte;
+                if (tc < g.N && tr < padm) g.qst[(int64_t)(tc / 32) * g.ldqst + tr / 32] = sbyte;
+            }
+        }
+        // the strip's 32 rows x 64 bytes as 16-byte row segments (LDS accesses of
+        // one wave complete in order, so the reads see the writes above)
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int rl = (lane >> 2) + 16 * k, chunk = lane & 3;
+            const uint4 w = *reinterpret_cast<const uint4 *>(strip + rl * kQPitch + 16 * chunk);
+            if (tr + rl < g.M && c0 + 32 * chunk < padn)
+                *reinterpret_cast<uint4 *>(g.qc + (int64_t)(tr + rl) * g.ldqc + c0 / 2 + 16 * chunk) = w;
+        }
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
 // SM: bit 0 -- A has 1x32 blocks (one scale per row and K-group: activations
 // in the forward GEMM), bit 1 -- B has them (activations in the weight-gradient
 // GEMM).  Such an operand's per-row scale words follow the 2D words in each
 // stage (1 KB per operand, one load per wave) and every lane reads its own
 // row's word instead of the block row's.
-template <bool BF16OUT, bool ACC, int GMODE, int SM>
+template <bool BF16OUT, bool ACC, int GMODE, int SM, bool QOUT = false>
 __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmArgs g, int tiles_m, int tiles_n,
                                                                           const GroupedArgs gr)
 {
@@ -475,6 +622,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];
     __shared__ int32_t pad_start[GMODE == 0 ? 1 : kMaxSegs + 1];
     __shared__ int32_t tile_start[GMODE == 1 ? kMaxSegs + 1 : 1];
+    __shared__ __attribute__((aligned(16))) uint8_t qstrip[QOUT ? 4 * kQStrip : 16];
 
     uint32_t total = (uint32_t)(tiles_m * tiles_n);
     if (GMODE != 0) {
@@ -509,11 +657,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
 
     auto store = [&](const TileRef &t) __attribute__((always_inline)) {
         const int r0 = t.m0 + wm * 128, c0 = t.n0 + wn * 128;
-        uint8_t *cb = t.c + (int64_t)r0 * ldc_bytes + (int64_t)c0 * esize;
-        if (t.m0 + BM2 <= t.M && t.n0 + BN2 <= t.N)
-            store_block<BF16OUT, ACC, false>(acc, cb, ldc_bytes, 128, 128);
-        else
-            store_block<BF16OUT, ACC, true>(acc, cb, ldc_bytes, t.M - r0, t.N - c0);
+        if constexpr (QOUT) {
+            uint8_t *strip = qstrip + wave * kQStrip;
+            if (t.m0 + BM2 <= t.M && t.n0 + BN2 <= t.N)
+                store_qblock<false>(acc, g, strip, r0, c0, 128, 128);
+            else
+                store_qblock<true>(acc, g, strip, r0, c0, t.M - r0, t.N - c0);
+        } else {
+            uint8_t *cb = t.c + (int64_t)r0 * ldc_bytes + (int64_t)c0 * esize;
+            if (t.m0 + BM2 <= t.M && t.n0 + BN2 <= t.N)
+                store_block<BF16OUT, ACC, false>(acc, cb, ldc_bytes, 128, 128);
+            else
+                store_block<BF16OUT, ACC, true>(acc, cb, ldc_bytes, t.M - r0, t.N - c0);
+        }
     };
 
     // ragged K: experts without rows give zero tiles (unchanged when accumulating)
@@ -945,6 +1101,37 @@ hipError_t launch_gemm(const GemmArgs &g, int fmt, int c_is_bf16, hipStream_t st
         return hipGetLastError();
     }
     return c_is_bf16 ? launch_t<kFmtMxfp8, true>(g, stream) : launch_t<kFmtMxfp8, false>(g, stream);
+}
+
+hipError_t launch_gemm_quantized(const GemmArgs &g, hipStream_t stream)
+{
+    const bool off32 = g.M * g.lda <= (int64_t(1) << 32) && g.N * g.ldb <= (int64_t(1) << 32);
+    if (!off32) return hipErrorInvalidValue;
+    const GroupedArgs none = {nullptr, 0, 0, 0, 0, 0};
+    const int tm = (int)((g.M + BM2 - 1) / BM2), tn = (int)((g.N + BN2 - 1) / BN2);
+    int64_t grid = cu_count();
+    const int64_t tiles = (int64_t)tm * tn;
+    grid = grid < tiles ? grid : tiles;
+    grid = (grid + kXcds - 1) / kXcds * kXcds;
+    switch ((g.a1d ? 1 : 0) | (g.b1d ? 2 : 0)) {
+    case 0:
+        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<false, false, 0, 0, true>), dim3((unsigned)grid), dim3(kThreads),
+                           0, stream, g, tm, tn, none);
+        break;
+    case 1:
+        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<false, false, 0, 1, true>), dim3((unsigned)grid), dim3(kThreads),
+                           0, stream, g, tm, tn, none);
+        break;
+    case 2:
+        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<false, false, 0, 2, true>), dim3((unsigned)grid), dim3(kThreads),
+                           0, stream, g, tm, tn, none);
+        break;
+    default:
+        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<false, false, 0, 3, true>), dim3((unsigned)grid), dim3(kThreads),
+                           0, stream, g, tm, tn, none);
+        break;
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_grouped_gemm(const GemmArgs &g, const GroupedArgs &gr, int c_is_bf16, hipStream_t stream)

@@ -47,9 +47,18 @@ struct GemmArgs {
     int64_t M, N, K;                    // K rounded up to 128
     int accumulate;
     int a1d, b1d;                       // FP4: operand with one scale per row and K-group (1x32 blocks)
+    // quantized output (FP4 GEMM only): C in 2D-block FP4, both orientations
+    // (the layout of a q2d_tensor), round to nearest; c is then unused
+    uint8_t *qc;  int64_t ldqc;         // codes [M][ldqc]
+    uint8_t *qct; int64_t ldqct;        // codes_t [N][ldqct]
+    uint8_t *qs;  int64_t ldqs;         // scales [ceil(M/32)][ldqs]
+    uint8_t *qst; int64_t ldqst;        // scales_t [ceil(N/32)][ldqst]
 };
 
 enum GemmFmt { kFmtFp4Block2D = 0, kFmtMxfp8 = 1 };
+
+// C = op(A) op(B)^T quantized to 2D-block FP4 in the epilogue (g.qc .. set)
+hipError_t launch_gemm_quantized(const GemmArgs &g, hipStream_t stream);
 
 hipError_t launch_gemm(const GemmArgs &g, int fmt, int c_is_bf16, hipStream_t stream);
 

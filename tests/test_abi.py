@@ -139,6 +139,32 @@ def test_block64_descriptors(q2d):
     assert L.q2d_gemm(ctypes.byref(d), 0, ctypes.byref(f), 0, fake, 0, 64, 0, None) == 1
 
 
+def test_gemm_quantized_error_paths(q2d):
+    L = q2d._lib
+    sizes = (ctypes.c_int64 * 4)()
+    fake = 0x1000
+    def t(fmt, R, C, block=32, bufs=True):
+        d = q2d._Tensor()
+        assert L.q2d_tensor_init(ctypes.byref(d), fmt, R, C, block, sizes) == 0
+        if bufs:
+            d.codes, d.scales, d.codes_t, d.scales_t = fake, fake, fake, fake
+        return d
+    a, b, out = t(0, 64, 96), t(0, 128, 96), t(0, 64, 128)
+    P = ctypes.byref
+    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 1, P(out), None) == 2          # SR
+    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 5, P(out), None) == 1          # bad mode
+    assert L.q2d_gemm_quantized(None, 0, P(b), 0, 0, P(out), None) == 1
+    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 0, None, None) == 1
+    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 0, P(t(0, 64, 127)), None) == 1   # shape
+    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 0, P(t(0, 64, 128, 64)), None) == 2  # block 64 output
+    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 0, P(t(2, 64, 128)), None) == 1   # 1D output
+    assert L.q2d_gemm_quantized(P(t(1, 64, 96)), 0, P(t(1, 128, 96)), 0, 0, P(out), None) == 2   # MXFP8
+    nt = t(0, 64, 128)
+    nt.codes_t, nt.scales_t = None, None
+    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 0, P(nt), None) == 1             # both orientations needed
+    assert L.q2d_gemm_quantized(P(a), 0, P(b), 1, 0, P(out), None) == 1            # K mismatch
+
+
 def test_dequantize_error_paths(q2d):
     L = q2d._lib
     sizes = (ctypes.c_int64 * 4)()
