@@ -53,6 +53,11 @@ WORKLOAD_TEXT = {
     "dense_7b_b64": "7B-class dense linears fwd+bwd (shapes and tensors of dense_7b) with 64x64 "
                     "2D-block FP4 for X, W and dY (the larger block of the block-size trade-off; "
                     "X, W round-to-nearest; dY stochastic)",
+    "dense_7b_yq_fused": "7B-class dense linears fwd+bwd (shapes and tensors of dense_7b) with every forward "
+                         "output Y delivered in 32x32 2D-block FP4 (round to nearest) for the next GEMM, "
+                         "quantized in the forward GEMM's epilogue",
+    "dense_7b_yq_separate": "the dense_7b_yq_fused step with Y written in bf16 by the forward GEMM and "
+                            "quantized by a separate quantizer launch",
     "mixed_7b": "7B-class block fwd+bwd, tokens 16384: Q/K projections in MXFP8 (E4M3, 1x32) "
                 "and V, O, gate, up, down in 32x32 2D-block FP4 with stochastic rounding; "
                 "bf16 inputs with outlier channels",
@@ -60,6 +65,7 @@ WORKLOAD_TEXT = {
 
 # what each kind of launch is measured against
 KIND_PEAK = {"gemm_fp4": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
+             "gemm_fp4_yq": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
              "gemm_fp4_grouped": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
              "gemm_fp8": ("mfma", PEAK_FP8_TFLOPS, "TFLOP/s"),
              "quant_fp4": ("hbm", PEAK_HBM_GBS, "GB/s"),
@@ -67,6 +73,7 @@ KIND_PEAK = {"gemm_fp4": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
              "quant_fp4_1d": ("hbm", PEAK_HBM_GBS, "GB/s"),
              "quant_mxfp8": ("hbm", PEAK_HBM_GBS, "GB/s")}
 KIND_KERNEL = {"gemm_fp4": "gemm_fp4_persistent_kernel", "gemm_fp4_grouped": "gemm_fp4_persistent_kernel (grouped)",
+               "gemm_fp4_yq": "gemm_fp4_persistent_kernel (FP4-quantizing epilogue)",
                "gemm_fp8": "gemm_fp8_256_kernel", "quant_fp4": "fp4_quantize_kernel",
                "quant_fp4_grouped": "fp4_quantize_kernel (grouped)",
                "quant_fp4_1d": "fp4_quantize_kernel (1D blocks)",
@@ -79,7 +86,8 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="dense_7b", choices=sorted(WORKLOAD_TEXT))
-    p.add_argument("--also", default="moe_30b,mixed_7b,dense_7b_1d,dense_7b_b64",
+    p.add_argument("--also", default="moe_30b,mixed_7b,dense_7b_1d,dense_7b_b64,dense_7b_yq_fused,"
+                                     "dense_7b_yq_separate",
                    help="further workloads measured in the same run (comma list, or 'none')")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-tokens", type=int, default=256)
@@ -122,7 +130,7 @@ def gemm_bytes(a_elems, b_elems, c_bytes, fmt="fp4", a1d=False, b1d=False) -> fl
             b_elems * (0.5 + (1.0 / 32.0 if b1d else 1.0 / 1024.0)) + c_bytes)
 
 
-KIND_SOURCES = {"gemm_fp4": "gemm.hip", "gemm_fp4_grouped": "gemm.hip", "gemm_fp8": "gemm.hip",
+KIND_SOURCES = {"gemm_fp4": "gemm.hip", "gemm_fp4_grouped": "gemm.hip", "gemm_fp8": "gemm.hip", "gemm_fp4_yq": "gemm.hip",
                 "quant_fp4": "quantize_fp4.hip", "quant_fp4_grouped": "quantize_fp4.hip",
                 "quant_fp4_1d": "quantize_fp4.hip", "quant_mxfp8": "quantize_mxfp8.hip"}
 
@@ -136,7 +144,11 @@ def kind_of(kernel_name: str):
     import re
     m = re.search(r"gemm_fp4_persistent_kernel<([^>]*)>", kernel_name)
     if m:
-        return "gemm_fp4" if m.group(1).split(",")[2].strip() == "0" else "gemm_fp4_grouped"
+        # template arguments: bf16 output, accumulate, grouped mode, 1D operands, quantized output
+        a = [t.strip() for t in m.group(1).split(",")]
+        if len(a) > 4 and a[4] == "true":
+            return "gemm_fp4_yq"
+        return "gemm_fp4" if a[2] == "0" else "gemm_fp4_grouped"
     if "gemm_fp8_256_kernel" in kernel_name:
         return "gemm_fp8"
     m = re.search(r"gemm_kernel<(\d)", kernel_name)
@@ -235,14 +247,27 @@ class Step:
             f = 2.0 * lin.tokens * lin.n_out * lin.k_in
             kind = "gemm_fp8" if lin.fmt == "mxfp8" else "gemm_fp4"
             T, N, K = lin.tokens, lin.n_out, lin.k_in
+            y_out = w.extra.get("y_out")
             for nm, a, ta, b, tb, out, mnk, a1, b1 in (("fwd", qx, 0, qw, 0, Y, (T, N, K), x1d, False),
                                                        ("dX", qdy, 0, qw, 1, dX, (T, K, N), False, False),
                                                        ("dW", qdy, 1, qx, 1, dW, (N, K, T), False, x1d)):
                 M_, N_, K_ = mnk
+                if nm == "fwd" and y_out == "fused":
+                    # Y leaves the epilogue as both FP4 layouts and the scale grids
+                    qy = q2d.QTensor(q2d.FP4_2D, T, N, dev)
+                    ab = gemm_bytes(M_ * K_, N_ * K_, M_ * N_ * (1.0 + 2.0 / 1024.0), lin.fmt, a1, b1)
+                    self.ops.append(("gemm_fp4_yq", "%s.%s" % (lin.name, nm), f, ab,
+                                     lambda a=a, b=b, qy=qy: q2d.q2d_gemm_quantized(a, 0, b, 0, "rtn", out=qy)))
+                    continue
                 ab = gemm_bytes(M_ * K_, N_ * K_, out.numel() * out.element_size(), lin.fmt, a1, b1)
                 self.ops.append((kind, "%s.%s" % (lin.name, nm), f, ab,
                                  lambda a=a, ta=ta, b=b, tb=tb, out=out:
                                  q2d.q2d_gemm(a, ta, b, tb, out=out)))
+                if nm == "fwd" and y_out == "separate":
+                    qy = q2d.QTensor(q2d.FP4_2D, T, N, dev)
+                    qb = quant_bytes(Y)
+                    self.ops.append(("quant_fp4", "%s.Y" % lin.name, qb, qb,
+                                     lambda Y=Y, qy=qy: q2d.q2d_quantize(Y, "rtn", out=qy)))
         self.flops = float(w.gemm_flops)
 
     def _moe(self):
@@ -368,7 +393,7 @@ def cpu_baseline(w, tokens: int):
                       "%.3f TFLOP" % (len(w.linears), tokens, dt, flops / 1e12)}
 
 
-PROFILE_WORKLOADS = ("dense_7b", "moe_30b", "mixed_7b", "dense_7b_1d", "dense_7b_b64")
+PROFILE_WORKLOADS = ("dense_7b", "moe_30b", "mixed_7b", "dense_7b_1d", "dense_7b_b64", "dense_7b_yq_fused")
 PROFILE_FILES = {
     "dense_7b": [("gemm_fp4_persistent_kernel.dense_7b.md", ("gemm_fp4",)),
                  ("fp4_quantize_kernel.dense_7b.md", ("quant_fp4",))],
@@ -376,12 +401,14 @@ PROFILE_FILES = {
     "dense_7b_1d": [("fp4_1d_kernels.dense_7b_1d.md", ("quant_fp4_1d", "gemm_fp4", "quant_fp4"))],
     "mixed_7b": [("mxfp8_kernels.mixed_7b.md", ("gemm_fp8", "quant_mxfp8", "gemm_fp4", "quant_fp4"))],
     "dense_7b_b64": [("block64_kernels.dense_7b_b64.md", ("quant_fp4", "gemm_fp4"))],
+    "dense_7b_yq_fused": [("gemm_fp4_yq.dense_7b_yq_fused.md", ("gemm_fp4_yq", "gemm_fp4", "quant_fp4"))],
+    "dense_7b_yq_separate": [("gemm_fp4_yq.dense_7b_yq_separate.md", ("gemm_fp4", "quant_fp4"))],
 }
 PROFILE_COMMANDS = """cd /tmp && export TMPDIR=/tmp; R=/root/repo; O=$R/gpurun_out/pb
 rocprofv3 --kernel-trace --stats --output-format csv -d $O/trace -o bench -- python3 $R/bench.py > $O/bench_trace.log 2>&1
 for c in FETCH_SIZE WRITE_SIZE; do
   rocprofv3 --pmc $c --output-format csv -d $O/copy_$c -o copy -- python3 $R/bench.py --copy-calibration 1073741824 > $O/copy_$c.log 2>&1
-  for wl in dense_7b moe_30b mixed_7b dense_7b_1d dense_7b_b64; do
+  for wl in dense_7b moe_30b mixed_7b dense_7b_1d dense_7b_b64 dense_7b_yq_fused; do
     rocprofv3 --pmc $c --output-format csv -d $O/${wl}_$c -o $wl -- python3 $R/bench.py --workload $wl --also none --steps 1 --warmup 0 --no-cpu-baseline > $O/${wl}_$c.log 2>&1
   done
 done

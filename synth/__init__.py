@@ -28,7 +28,7 @@ import torch
 
 __all__ = [
     "normal", "add_outlier_channels", "moe_counts", "segment_offsets",
-    "Workload", "student_t", "regression_task", "tiny", "dense_1b", "dense_7b", "dense_7b_1d", "dense_7b_b64", "moe_30b", "mixed_7b", "WORKLOADS",
+    "Workload", "student_t", "regression_task", "tiny", "dense_1b", "dense_7b", "dense_7b_1d", "dense_7b_b64", "dense_7b_yq", "moe_30b", "mixed_7b", "WORKLOADS",
 ]
 
 
@@ -227,6 +227,16 @@ def dense_7b_b64(device="cpu") -> Workload:
     return w
 
 
+def dense_7b_yq(device="cpu", fused: bool = True) -> Workload:
+    """The dense_7b tensors and linears with every forward output Y delivered in
+    2D-block FP4 (round to nearest) for the next GEMM: quantized in the forward
+    GEMM's epilogue (fused) or by a separate quantization of the bf16 Y."""
+    w = dense_7b(device)
+    w.extra["y_out"] = "fused" if fused else "separate"
+    w.name = "dense_7b_yq_fused" if fused else "dense_7b_yq_separate"
+    return w
+
+
 def mixed_7b(device="cpu") -> Workload:
     """7B block with Q/K projections in MXFP8 and V, O, gate, up, down in 2D-block FP4 (SR)."""
     T, H, F = 16384, 4096, 11008
@@ -269,4 +279,6 @@ def moe_30b(device="cpu", tokens: int = 16384, experts: int = 128, topk: int = 8
 
 
 WORKLOADS = {"tiny": tiny, "dense_1b": dense_1b, "dense_7b": dense_7b, "dense_7b_1d": dense_7b_1d,
-             "dense_7b_b64": dense_7b_b64, "moe_30b": moe_30b, "mixed_7b": mixed_7b}
+             "dense_7b_b64": dense_7b_b64, "moe_30b": moe_30b, "mixed_7b": mixed_7b,
+             "dense_7b_yq_fused": lambda device="cpu": dense_7b_yq(device, True),
+             "dense_7b_yq_separate": lambda device="cpu": dense_7b_yq(device, False)}
