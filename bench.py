@@ -67,12 +67,16 @@ WORKLOAD_TEXT = {
 KIND_PEAK = {"gemm_fp4": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
              "gemm_fp4_yq": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
              "gemm_fp4_grouped": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
+             # ragged-K weight gradients: per expert a short K and a float32 output
+             # of E x N x K_in, so the output writes bound them
+             "gemm_fp4_grouped_k": ("hbm", PEAK_HBM_GBS, "GB/s"),
              "gemm_fp8": ("mfma", PEAK_FP8_TFLOPS, "TFLOP/s"),
              "quant_fp4": ("hbm", PEAK_HBM_GBS, "GB/s"),
              "quant_fp4_grouped": ("hbm", PEAK_HBM_GBS, "GB/s"),
              "quant_fp4_1d": ("hbm", PEAK_HBM_GBS, "GB/s"),
              "quant_mxfp8": ("hbm", PEAK_HBM_GBS, "GB/s")}
 KIND_KERNEL = {"gemm_fp4": "gemm_fp4_persistent_kernel", "gemm_fp4_grouped": "gemm_fp4_persistent_kernel (grouped)",
+               "gemm_fp4_grouped_k": "gemm_fp4_persistent_kernel (grouped, ragged K)",
                "gemm_fp4_yq": "gemm_fp4_persistent_kernel (FP4-quantizing epilogue)",
                "gemm_fp8": "gemm_fp8_256_kernel", "quant_fp4": "fp4_quantize_kernel",
                "quant_fp4_grouped": "fp4_quantize_kernel (grouped)",
@@ -130,7 +134,7 @@ def gemm_bytes(a_elems, b_elems, c_bytes, fmt="fp4", a1d=False, b1d=False) -> fl
             b_elems * (0.5 + (1.0 / 32.0 if b1d else 1.0 / 1024.0)) + c_bytes)
 
 
-KIND_SOURCES = {"gemm_fp4": "gemm.hip", "gemm_fp4_grouped": "gemm.hip", "gemm_fp8": "gemm.hip", "gemm_fp4_yq": "gemm.hip",
+KIND_SOURCES = {"gemm_fp4": "gemm.hip", "gemm_fp4_grouped": "gemm.hip", "gemm_fp4_grouped_k": "gemm.hip", "gemm_fp8": "gemm.hip", "gemm_fp4_yq": "gemm.hip",
                 "quant_fp4": "quantize_fp4.hip", "quant_fp4_grouped": "quantize_fp4.hip",
                 "quant_fp4_1d": "quantize_fp4.hip", "quant_mxfp8": "quantize_mxfp8.hip"}
 
@@ -148,7 +152,7 @@ def kind_of(kernel_name: str):
         a = [t.strip() for t in m.group(1).split(",")]
         if len(a) > 4 and a[4] == "true":
             return "gemm_fp4_yq"
-        return "gemm_fp4" if a[2] == "0" else "gemm_fp4_grouped"
+        return {"0": "gemm_fp4", "1": "gemm_fp4_grouped"}.get(a[2], "gemm_fp4_grouped_k")
     if "gemm_fp8_256_kernel" in kernel_name:
         return "gemm_fp8"
     m = re.search(r"gemm_kernel<(\d)", kernel_name)
@@ -300,7 +304,8 @@ class Step:
             out = torch.empty(shape, dtype=dt, device=dev)
             ab = gemm_bytes(w.tensors[a].numel(), w.tensors[b].numel(),
                             out.numel() * out.element_size(), "fp4")
-            self.ops.append(("gemm_fp4_grouped", nm, f, ab,
+            ragged_k = ta == 1 and tb == 1
+            self.ops.append(("gemm_fp4_grouped_k" if ragged_k else "gemm_fp4_grouped", nm, ab if ragged_k else f, ab,
                              lambda a=qt[a], ta=ta, b=qt[b], tb=tb, out=out:
                              q2d.q2d_grouped_gemm(a, ta, b, tb, off, out=out)))
             self.flops += f
@@ -397,7 +402,8 @@ PROFILE_WORKLOADS = ("dense_7b", "moe_30b", "mixed_7b", "dense_7b_1d", "dense_7b
 PROFILE_FILES = {
     "dense_7b": [("gemm_fp4_persistent_kernel.dense_7b.md", ("gemm_fp4",)),
                  ("fp4_quantize_kernel.dense_7b.md", ("quant_fp4",))],
-    "moe_30b": [("grouped_fp4_kernels.moe_30b.md", ("gemm_fp4_grouped", "quant_fp4_grouped", "quant_fp4"))],
+    "moe_30b": [("grouped_fp4_kernels.moe_30b.md", ("gemm_fp4_grouped", "gemm_fp4_grouped_k", "quant_fp4_grouped",
+                                                    "quant_fp4"))],
     "dense_7b_1d": [("fp4_1d_kernels.dense_7b_1d.md", ("quant_fp4_1d", "gemm_fp4", "quant_fp4"))],
     "mixed_7b": [("mxfp8_kernels.mixed_7b.md", ("gemm_fp8", "quant_mxfp8", "gemm_fp4", "quant_fp4"))],
     "dense_7b_b64": [("block64_kernels.dense_7b_b64.md", ("quant_fp4", "gemm_fp4"))],
@@ -447,6 +453,15 @@ def _counter_means(dirname, counter):
     return {k: (v[0] / v[1], v[1]) for k, v in acc.items()}
 
 
+def phase_owners(n_rows: int, phases) -> list:
+    """Workload of each libq2d dispatch of a trace, in dispatch order: the workloads
+    run one after the other and each reports how many dispatches it made."""
+    total = sum(n for _, n in phases)
+    if n_rows != total:
+        raise ValueError("trace holds %d libq2d dispatches, the run reports %d" % (n_rows, total))
+    return [wl for wl, n in phases for _ in range(n)]
+
+
 def summarize_profiles(d: str, out_dir: str):
     """Turn the rocprofv3 outputs of PROFILE_COMMANDS into the text summaries of
     `out_dir`: per-kernel duration statistics next to the benchmark's own HIP-event
@@ -488,10 +503,7 @@ def summarize_profiles(d: str, out_dir: str):
     rows = _csv(os.path.join(d, "trace"), "_kernel_trace.csv")
     rows.sort(key=lambda r: int(r["Dispatch_Id"]))
     rows = [r for r in rows if kind_of(r["Kernel_Name"]) is not None]
-    if len(rows) != sum(n for _, n in phases):
-        raise ValueError("trace holds %d libq2d dispatches, the run reports %d"
-                         % (len(rows), sum(n for _, n in phases)))
-    owner = [wl for wl, n in phases for _ in range(n)]
+    owner = phase_owners(len(rows), phases)
     durs = {}
     for r, phase in zip(rows, owner):
         kind = kind_of(r["Kernel_Name"])
