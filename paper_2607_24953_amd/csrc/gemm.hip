@@ -24,6 +24,20 @@
 
 namespace q2d {
 
+// compute units of the current device (queried once per device)
+int cu_count()
+{
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int n = cache[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cache[dev].store(n, std::memory_order_relaxed);
+    }
+    return n;
+}
+
 namespace {
 
 constexpr int BM = 128, BN = 128, BK = 128;
@@ -1022,19 +1036,6 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
     }
 }
 
-// compute units of the current device (queried once per device)
-int cu_count()
-{
-    static std::atomic<int> cache[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    int n = cache[dev].load(std::memory_order_relaxed);
-    if (n == 0) {
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-        cache[dev].store(n, std::memory_order_relaxed);
-    }
-    return n;
-}
 
 // persistent kernel over at most `tiles` tiles: one workgroup per CU, a
 // multiple of 8 (the XCD count) so that every workgroup stays on one XCD's

@@ -6,6 +6,9 @@
 
 namespace q2d {
 
+// compute units of the current device (queried once per device)
+int cu_count();
+
 // One 2D-block FP4 or MXFP8 quantization launch over an R x C matrix whose
 // element (r, c) sits at x[r*stride_r + c*stride_c].
 struct QuantArgs {

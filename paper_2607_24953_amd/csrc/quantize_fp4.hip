@@ -117,15 +117,16 @@ __device__ __forceinline__ void philox_block(uint64_t g, uint32_t o0, uint32_t o
     w[0] = c0; w[1] = c1; w[2] = c2; w[3] = c3;
 }
 
+// One 128-row tile (row tile tr, column tile tc) of the quantization described
+// by `a` (for a grouped tensor, `a` is already narrowed to the tile's segment).
 // VEC: rows are read as aligned 8-element vectors (stride_c == 1).
 // SR: stochastic rounding.  ALIGNED8: every sub-block row starts at a storage
 // index that is a multiple of 8, so one Philox block serves its 8 elements.
 // GROUPED: the rows are expert segments (see QuantArgs).  WC: 128-column
 // strips per tile (waves side by side).  ONED: 1 x 32 / 32 x 1 blocks.
 template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED, int WC, bool ONED>
-__global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
+__device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, const int64_t tc)
 {
-    static_assert(!(ONED && GROUPED), "grouped tensors use 2D blocks");
     constexpr int kTC = 128 * WC;
     constexpr int kThreads = 256 * WC;
     constexpr bool PK = sizeof(T) == 2;     // bf16: two elements per register
@@ -133,33 +134,6 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int wr = wave / WC, wc = wave % WC;
-    const int64_t tiles_c = (a.cols_pad + kTC - 1) / kTC;
-    const int64_t tile = blockIdx.x;
-    int64_t tr = tile / tiles_c;
-    const int64_t tc = tile - tr * tiles_c;
-    if (GROUPED) {
-        // padded start rows of the segments; this tile's segment and its local row tile
-        __shared__ int32_t pad_start[kMaxSegs + 1];
-        const int64_t *off = a.seg_offsets;
-        if (wave == 0)
-            wave_prefix(a.nseg, [&](int i) { return (int32_t)((off[i + 1] - off[i] + 127) / 128 * 128); }, pad_start);
-        __syncthreads();
-        const int32_t prow = (int32_t)(tr * kTile);
-        if (prow >= pad_start[a.nseg]) return;
-        const int e = seg_search(pad_start, a.nseg, prow);
-        const int64_t r_begin = off[e], n_e = off[e + 1] - off[e];
-        const int32_t p_e = pad_start[e];
-        tr = (prow - p_e) / kTile;
-        a.x = reinterpret_cast<const uint8_t *>(a.x) + r_begin * a.stride_r * (int64_t)sizeof(T);
-        a.index_base += r_begin * a.stride_r;
-        a.rows = n_e;
-        a.store_rows = (n_e + 127) / 128 * 128;
-        a.nbr = a.store_rows / 32;
-        if (a.codes) a.codes += (int64_t)p_e * a.ld_codes;
-        if (a.codes_t) a.codes_t += p_e / 2;
-        if (a.scales) a.scales += (int64_t)(p_e / 32) * a.ld_scales;
-        if (a.scales_t) a.scales_t += p_e / 32;
-    }
     const int64_t strip_r = tr * kTile + wr * 32;
     const int rg = lane >> 4, cc = lane & 15;
     const int64_t r0 = strip_r + 8 * rg;
@@ -517,6 +491,48 @@ __global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
     }
 }
 
+template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED, int WC, bool ONED>
+__global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
+{
+    static_assert(!(ONED && GROUPED), "grouped tensors use 2D blocks");
+    constexpr int kTC = 128 * WC;
+    const int64_t tiles_c = (a.cols_pad + kTC - 1) / kTC;
+    if constexpr (GROUPED) {
+        // padded start rows of the segments, built once per workgroup; the
+        // workgroup then walks the row tiles of all segments (tile = blockIdx.x,
+        // + gridDim.x, ...) and narrows `a` to each tile's segment
+        __shared__ int32_t pad_start[kMaxSegs + 1];
+        const int64_t *off = a.seg_offsets;
+        if ((threadIdx.x >> 6) == 0)
+            wave_prefix(a.nseg, [&](int i) { return (int32_t)((off[i + 1] - off[i] + 127) / 128 * 128); }, pad_start);
+        __syncthreads();
+        const int64_t tiles = (int64_t)(pad_start[a.nseg] / kTile) * tiles_c;
+        for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+            const int64_t rt = tile / tiles_c, tc = tile - rt * tiles_c;
+            const int32_t prow = (int32_t)(rt * kTile);
+            const int e = seg_search(pad_start, a.nseg, prow);
+            const int64_t r_begin = off[e], n_e = off[e + 1] - off[e];
+            const int32_t p_e = pad_start[e];
+            QuantArgs b = a;
+            b.x = reinterpret_cast<const uint8_t *>(a.x) + r_begin * a.stride_r * (int64_t)sizeof(T);
+            b.index_base += r_begin * a.stride_r;
+            b.rows = n_e;
+            b.store_rows = (n_e + 127) / 128 * 128;
+            b.nbr = b.store_rows / 32;
+            if (b.codes) b.codes += (int64_t)p_e * a.ld_codes;
+            if (b.codes_t) b.codes_t += p_e / 2;
+            if (b.scales) b.scales += (int64_t)(p_e / 32) * a.ld_scales;
+            if (b.scales_t) b.scales_t += p_e / 32;
+            quantize_tile<T, VEC, SR, ALIGNED8, GROUPED, WC, ONED>(b, (prow - p_e) / kTile, tc);
+            __syncthreads();                // the tile's LDS staging is reused by the next
+        }
+    } else {
+        const int64_t tile = blockIdx.x;
+        const int64_t tr = tile / tiles_c;
+        quantize_tile<T, VEC, SR, ALIGNED8, GROUPED, WC, ONED>(a, tr, tile - tr * tiles_c);
+    }
+}
+
 template <typename T, bool VEC, bool SR, bool A8, bool G, bool ONED>
 hipError_t launch_t(const QuantArgs &a, hipStream_t s)
 {
@@ -524,7 +540,10 @@ hipError_t launch_t(const QuantArgs &a, hipStream_t s)
     // 128-byte lines of codes.  Stochastic rounding is bound by its Philox work
     // and keeps 4-wave workgroups for occupancy.
     constexpr int WC = SR ? 1 : 2;
-    const int64_t nb = (a.rows_pad / kTile) * ((a.cols_pad + 128 * WC - 1) / (128 * WC));
+    int64_t nb = (a.rows_pad / kTile) * ((a.cols_pad + 128 * WC - 1) / (128 * WC));
+    // grouped: a few workgroups per CU walk the tiles, so that each builds the
+    // segment table once (the bound covers every padded segment's tiles)
+    if (G) nb = nb < 4 * (int64_t)cu_count() ? nb : 4 * (int64_t)cu_count();
     hipLaunchKernelGGL((fp4_quantize_kernel<T, VEC, SR, A8, G, WC, ONED>), dim3((unsigned)nb), dim3(256 * WC), 0, s,
                        a);
     return hipGetLastError();
