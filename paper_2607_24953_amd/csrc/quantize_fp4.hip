@@ -491,8 +491,11 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
     }
 }
 
+// Vector-load stochastic-rounding variants at most 168 VGPRs (three waves per
+// SIMD): they are bound by their Philox arithmetic and need the occupancy to
+// hide its latency (the grouped one would otherwise take 169 and drop to two).
 template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED, int WC, bool ONED>
-__global__ __launch_bounds__(256 * WC) void fp4_quantize_kernel(QuantArgs a)
+__global__ __launch_bounds__(256 * WC) __attribute__((amdgpu_waves_per_eu(VEC && SR ? 3 : 1))) void fp4_quantize_kernel(QuantArgs a)
 {
     static_assert(!(ONED && GROUPED), "grouped tensors use 2D blocks");
     constexpr int kTC = 128 * WC;
@@ -541,9 +544,10 @@ hipError_t launch_t(const QuantArgs &a, hipStream_t s)
     // and keeps 4-wave workgroups for occupancy.
     constexpr int WC = SR ? 1 : 2;
     int64_t nb = (a.rows_pad / kTile) * ((a.cols_pad + 128 * WC - 1) / (128 * WC));
-    // grouped: a few workgroups per CU walk the tiles, so that each builds the
-    // segment table once (the bound covers every padded segment's tiles)
-    if (G) nb = nb < 4 * (int64_t)cu_count() ? nb : 4 * (int64_t)cu_count();
+    // grouped: each workgroup walks several tiles, so that the segment table is
+    // built once per few tiles (the bound covers every padded segment's tiles);
+    // 8 per CU keeps the last round of tiles short
+    if (G) nb = nb < 8 * (int64_t)cu_count() ? nb : 8 * (int64_t)cu_count();
     hipLaunchKernelGGL((fp4_quantize_kernel<T, VEC, SR, A8, G, WC, ONED>), dim3((unsigned)nb), dim3(256 * WC), 0, s,
                        a);
     return hipGetLastError();
