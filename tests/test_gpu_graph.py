@@ -1,0 +1,73 @@
+"""The library under HIP graph capture: a quantized linear layer's forward and
+backward (quantizers and GEMMs, including the quantizing epilogue) captured on
+torch's current stream, replayed several times with eager work and
+synchronisations in between; every replay must reproduce the eager results
+bit for bit (the kernels are deterministic: no atomics, fixed reduction
+order).  The library allocates nothing and issues no memset, so nothing in a
+captured call depends on host state.
+"""
+import pytest
+import torch
+
+import synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module")
+def q2d():
+    import paper_2607_24953_amd as q
+    return q
+
+
+def test_linear_layer_graph_replays(q2d):
+    T, N, K = 512, 768, 640
+    X = synth.normal((T, K), 1.0, 81, torch.bfloat16, device=DEV)
+    W = synth.normal((N, K), 0.02, 82, torch.bfloat16, device=DEV)
+    dY = synth.normal((T, N), 1e-3, 83, torch.bfloat16, device=DEV)
+    qX = q2d.QTensor(q2d.FP4_2D, T, K, DEV)
+    qW = q2d.QTensor(q2d.FP4_2D, N, K, DEV)
+    qdY = q2d.QTensor(q2d.FP4_2D, T, N, DEV)
+    qY = q2d.QTensor(q2d.FP4_2D, T, N, DEV)
+    Y = torch.empty((T, N), dtype=torch.float32, device=DEV)
+    dX = torch.empty((T, K), dtype=torch.bfloat16, device=DEV)
+    dW = torch.empty((N, K), dtype=torch.float32, device=DEV)
+
+    def step():
+        q2d.q2d_linear_fwd(X, W, "rtn", "rtn", 5, 0, 1, torch.float32, qX=qX, qW=qW, Y=Y)
+        q2d.q2d_linear_bwd(dY, qX, qW, "sr", 5, 2, torch.bfloat16, torch.float32, dW=dW, qdY=qdY, dX=dX)
+        q2d.q2d_gemm_quantized(qX, 0, qW, 0, "rtn", out=qY)
+
+    def snapshot():
+        torch.cuda.synchronize()
+        out = {"Y": Y.clone(), "dX": dX.clone(), "dW": dW.clone()}
+        for name, q in (("qX", qX), ("qW", qW), ("qdY", qdY), ("qY", qY)):
+            for k in ("codes", "codes_t", "scales", "scales_t"):
+                out[name + "." + k] = getattr(q, k).clone()
+        return out
+
+    step()
+    want = snapshot()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()                                         # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(s)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for rep in range(3):
+        for t in (Y, dX, dW):
+            t.fill_(float("nan"))
+        for q in (qX, qW, qdY, qY):
+            q.codes.fill_(0xAA)
+            q.codes_t.fill_(0xAA)
+        torch.cuda.synchronize()
+        _ = torch.randn(1000, device=DEV).sum().item()    # eager work between replays
+        g.replay()
+        got = snapshot()
+        for k, v in want.items():
+            assert torch.equal(got[k].view(torch.uint8) if got[k].dtype != torch.uint8 else got[k],
+                               v.view(torch.uint8) if v.dtype != torch.uint8 else v), (rep, k)
