@@ -410,7 +410,7 @@ PROFILE_FILES = {
     "dense_7b_yq_fused": [("gemm_fp4_yq.dense_7b_yq_fused.md", ("gemm_fp4_yq", "gemm_fp4", "quant_fp4"))],
     "dense_7b_yq_separate": [("gemm_fp4_yq.dense_7b_yq_separate.md", ("gemm_fp4", "quant_fp4"))],
 }
-PROFILE_COMMANDS = """cd /tmp && export TMPDIR=/tmp; R=/root/repo; O=$R/gpurun_out/pb
+PROFILE_COMMANDS = """cd /tmp && export TMPDIR=/tmp; R=/root/repo; O=${PROFILE_OUT:-$R/profile_runs}; mkdir -p $O
 rocprofv3 --kernel-trace --stats --output-format csv -d $O/trace -o bench -- python3 $R/bench.py > $O/bench_trace.log 2>&1
 for c in FETCH_SIZE WRITE_SIZE; do
   rocprofv3 --pmc $c --output-format csv -d $O/copy_$c -o copy -- python3 $R/bench.py --copy-calibration 1073741824 > $O/copy_$c.log 2>&1
