@@ -418,7 +418,10 @@ for c in FETCH_SIZE WRITE_SIZE; do
     rocprofv3 --pmc $c --output-format csv -d $O/${wl}_$c -o $wl -- python3 $R/bench.py --workload $wl --also none --steps 1 --warmup 0 --no-cpu-baseline > $O/${wl}_$c.log 2>&1
   done
 done
+rocprofv3 --pmc MfmaUtil LdsUtil LDSBankConflict LdsBankConflict --output-format csv -d $O/dense_7b_util -o dense_7b -- python3 $R/bench.py --workload dense_7b --also none --steps 1 --warmup 0 --no-cpu-baseline > $O/dense_7b_util.log 2>&1
+rocprofv3 --pmc TCC_HIT_sum TCC_MISS_sum --output-format csv -d $O/dense_7b_l2 -o dense_7b -- python3 $R/bench.py --workload dense_7b --also none --steps 1 --warmup 0 --no-cpu-baseline > $O/dense_7b_l2.log 2>&1
 python3 $R/bench.py --summarize-profiles $O"""
+
 
 
 def _json_line(path):
@@ -451,6 +454,53 @@ def _counter_means(dirname, counter):
             a = acc.setdefault(kind, [0.0, 0])
             a[0] += float(r["Counter_Value"]); a[1] += 1
     return {k: (v[0] / v[1], v[1]) for k, v in acc.items()}
+
+
+def _per_dispatch(dirname):
+    """{dispatch id: (kind, duration ns, {counter: value})} of a counter-collection run."""
+    out = {}
+    for r in _csv(dirname, "_counter_collection.csv"):
+        kind = kind_of(r["Kernel_Name"])
+        if kind is None:
+            continue
+        dur = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        k, _, cs = out.setdefault(int(r["Dispatch_Id"]), (kind, dur, {}))
+        cs[r["Counter_Name"]] = cs.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return out
+
+
+UTIL_COUNTERS = ("MfmaUtil", "LdsUtil", "LDSBankConflict", "LdsBankConflict", "TCC_HIT_sum", "TCC_MISS_sum")
+
+
+def utilisation(d: str) -> dict:
+    """Per kind of the dense 7B step, from the counter runs of PROFILE_COMMANDS:
+    rocprofv3's MfmaUtil (% of SIMD cycles with the MFMA unit busy), LdsUtil,
+    LDSBankConflict (% of GPU time LDS stalls on bank conflicts) and LdsBankConflict
+    (conflicts per access), each averaged over dispatches weighted by duration, and
+    the L2 hit rate TCC_HIT / (TCC_HIT + TCC_MISS)."""
+    acc = {}
+    for sub in ("dense_7b_util", "dense_7b_l2"):
+        path = os.path.join(d, sub)
+        if not os.path.isdir(path):
+            continue
+        for kind, dur, cs in _per_dispatch(path).values():
+            a = acc.setdefault(kind, {c: [0.0, 0.0] for c in UTIL_COUNTERS})
+            for c, v in cs.items():
+                if c in a:
+                    a[c][0] += v * (dur if not c.startswith("TCC") else 1.0)
+                    a[c][1] += dur if not c.startswith("TCC") else 1.0
+    out = {}
+    for kind, a in acc.items():
+        mean = {c: (v / w if w else None) for c, (v, w) in a.items()}
+        hit, miss = a["TCC_HIT_sum"][0], a["TCC_MISS_sum"][0]
+        out[kind] = {"mfma_util_pct": None if mean["MfmaUtil"] is None else round(mean["MfmaUtil"], 2),
+                     "lds_util_pct": None if mean["LdsUtil"] is None else round(mean["LdsUtil"], 2),
+                     "lds_bank_conflict_pct_time": None if mean["LDSBankConflict"] is None
+                     else round(mean["LDSBankConflict"], 2),
+                     "lds_bank_conflicts_per_access": None if mean["LdsBankConflict"] is None
+                     else round(mean["LdsBankConflict"], 4),
+                     "l2_hit_rate": round(hit / (hit + miss), 4) if hit + miss else None}
+    return out
 
 
 def phase_owners(n_rows: int, phases) -> list:
@@ -488,6 +538,9 @@ def summarize_profiles(d: str, out_dir: str):
                 "write_bytes_per_launch": round(wb), "algorithmic_bytes_per_launch": round(alg),
                 "traffic_over_algorithmic": round((fb + wb) / alg, 3), "launches": fetch[kind][1],
                 "source_hash": bj["source_hashes"][kind]}
+    util = utilisation(d)
+    if util:
+        traffic["_utilisation_dense_7b"] = util
     with open(os.path.join(out_dir, "traffic.json"), "w") as f:
         json.dump(traffic, f, indent=1, sort_keys=True)
         f.write("\n")
@@ -534,6 +587,19 @@ def summarize_profiles(d: str, out_dir: str):
                     out.append("| %s | %d | %d | %.3f |" % (kind, t["bytes_per_launch"],
                                                          t["algorithmic_bytes_per_launch"],
                                                          t["traffic_over_algorithmic"]))
+            if wl == "dense_7b" and util:
+                out += ["", "## MFMA and LDS utilisation, L2 hit rate (counter runs of this workload)", "",
+                        "rocprofv3 derived counters per dispatch, averaged weighted by duration: MfmaUtil, "
+                        "LdsUtil, LDSBankConflict (% of GPU time LDS stalls on bank conflicts), "
+                        "LdsBankConflict (conflicts per access); L2 hit rate = TCC_HIT / (TCC_HIT + TCC_MISS).",
+                        "", "| kind | MfmaUtil % | LdsUtil % | LDSBankConflict % | LdsBankConflict / access | "
+                        "L2 hit rate |", "|---|---|---|---|---|---|"]
+                for kind in kinds:
+                    u = util.get(kind)
+                    if u:
+                        out.append("| %s | %s | %s | %s | %s | %s |" % (
+                            kind, u["mfma_util_pct"], u["lds_util_pct"], u["lds_bank_conflict_pct_time"],
+                            u["lds_bank_conflicts_per_access"], u["l2_hit_rate"]))
             out += ["", "## rocprofv3 --stats rows of these kernels (whole benchmark run, all workloads)", "",
                     "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
             for r in stats:
