@@ -193,13 +193,15 @@ def _sample_rows(qt_np, trans, rows, fmt="fp4"):
     raise ValueError(fmt)
 
 
-def test_full_7b_launch_configuration(q2d):
-    """The benchmark's 15 GEMMs (bf16 Y and dX, fp32 dW) at full size, 48 sampled rows each.
+@pytest.mark.parametrize("name", ["dense_1b", "dense_7b"])
+def test_full_launch_configuration(q2d, name):
+    """Every GEMM of the 1B-class (SR on all operands) and 7B-class (the benchmark's
+    15) linear workloads at full size (bf16 Y and dX, fp32 dW), 48 sampled rows each.
 
     The oracle quantizes the same inputs (byte-equal to the device operands);
     the device GEMMs are compared with float64 products of the oracle's
     operands on sampled output rows."""
-    w = synth.dense_7b(device=DEV)
+    w = synth.WORKLOADS[name](device=DEV)
     rng = np.random.default_rng(0)
     for lin in w.linears:
         X, W, dY = w.tensors[lin.x], w.tensors[lin.w], w.tensors[lin.dy]
@@ -212,8 +214,8 @@ def test_full_7b_launch_configuration(q2d):
         ow = oracle.quantize_fp4_2d(W.cpu(), w.rounding[lin.w], w.seed, 1)
         ody = oracle.quantize_fp4_2d(dY.cpu(), w.rounding[lin.dy], w.seed, 2)
         for name, gq, oq in (("X", qX, ox), ("W", qW, ow), ("dY", qdY, ody)):
-            assert_same_bytes(gpu_buffers(gq), oq, "7B %s %s" % (lin.name, name))
-        print("7B linear %s: checking sampled rows" % lin.name, flush=True)
+            assert_same_bytes(gpu_buffers(gq), oq, "%s %s %s" % (w.name, lin.name, name))
+        print("%s linear %s: checking sampled rows" % (w.name, lin.name), flush=True)
         Wf = oracle.operand(ow, False)
         Wt = oracle.operand(ow, True)
         Xt = oracle.operand(ox, True)
