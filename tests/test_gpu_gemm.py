@@ -126,6 +126,25 @@ def test_gemm_unit_scales_exact(q2d):
     assert np.array_equal(c * 4, (ai @ bi.T).astype(np.float64))
 
 
+@pytest.mark.parametrize("M,N,K,ta,tb", [(300, 200, 160, 0, 0), (2100, 4000, 384, 0, 1), (4096, 2048, 640, 1, 1)])
+def test_gemm_non_finite_blocks(q2d, M, N, K, ta, tb):
+    """A NaN and an infinity in two blocks of A give those blocks scale 0xFF (NaN):
+    exactly the output entries whose dot product meets them are NaN, on the small and
+    the persistent kernel, and the rest match the oracle."""
+    A = synth.normal((K, M) if ta else (M, K), 1.0, 91, torch.float32)
+    B = synth.normal((K, N) if tb else (N, K), 0.02, 92, torch.float32)
+    A[5, 7] = float("nan")
+    A[-1, -1] = float("inf")
+    qa, oa = quant(q2d, A.to(DEV), "rtn")
+    qb, ob = quant(q2d, B.to(DEV), "rtn")
+    ref = oracle.gemm(oracle.operand(oa, bool(ta)), oracle.operand(ob, bool(tb)))
+    c = q2d.q2d_gemm(qa, ta, qb, tb, out_dtype=torch.float32).cpu().numpy().astype(np.float64)
+    nan = np.isnan(ref)
+    assert nan.any() and not nan.all()
+    assert np.array_equal(np.isnan(c), nan)
+    assert rel_frob(c[~nan], ref[~nan]) <= TOL
+
+
 @pytest.mark.parametrize("T,N,K", [(128, 256, 256), (96, 300, 200), (512, 1024, 768)])
 def test_linear_fwd_bwd(q2d, T, N, K):
     X = synth.normal((T, K), 1.0, 1, torch.bfloat16, device=DEV)
