@@ -11,12 +11,15 @@
 // what lets one quantization serve Y = X W^T, dX = dY W and dW = dY^T X.  For
 // MXFP8 each row has its own scale per K-group.
 //
-// Tiling: 256 threads, 128 x 128 output tile, 2 x 2 waves of 64 x 64 (2 x 2
-// MFMA tiles each), K-tile of 128 elements staged in LDS with double
-// buffering.  LDS rows are XOR-swizzled in 16-byte chunks so that the MFMA
-// operand reads (32 consecutive rows, same chunk) hit distinct banks.
-// Workgroups are remapped so that each XCD (one L2) walks a contiguous band of
-// output tiles, grouped by 8 row tiles for operand reuse.
+// Two kernels.  Problems with at least 128 output tiles of 256 x 256 run on the
+// persistent large-tile kernels further down (gemm_fp4_persistent_kernel, also
+// the grouped and quantized-output forms, and gemm_fp8_256_kernel).  Smaller
+// problems use gemm_kernel: 256 threads, 128 x 128 output tile, 2 x 2 waves of
+// 64 x 64 (2 x 2 MFMA tiles each), K-tile of 128 elements staged in LDS with
+// double buffering.  LDS rows are XOR-swizzled in 16-byte chunks (Fmt::swz) so
+// that the MFMA operand reads hit distinct banks.  Workgroups are remapped so
+// that each XCD (one L2) walks a contiguous band of output tiles, grouped by 8
+// row tiles for operand reuse.
 #include <atomic>
 #include <type_traits>
 #include "device_common.hpp"
