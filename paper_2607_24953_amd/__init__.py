@@ -146,6 +146,24 @@ def _check_input(x: torch.Tensor):
         raise Q2DError("expected a 2-D device tensor")
 
 
+def _norm(device) -> torch.device:
+    d = torch.device(device)
+    if d.type == "cuda" and d.index is None:
+        d = torch.device("cuda", torch.cuda.current_device())
+    return d
+
+
+def _same_device(device, *objs):
+    """Every tensor / QTensor in objs (None skipped) lives on `device`, a GPU: the
+    kernels write through these pointers, so a host buffer must not reach them."""
+    ref = _norm(device)
+    if ref.type != "cuda":
+        raise Q2DError("expected device tensors, got %s" % ref)
+    for o in objs:
+        if o is not None and _norm(o.device) != ref:
+            raise Q2DError("all operands must be on %s (got %s)" % (ref, o.device))
+
+
 def q2d_quantize(x: torch.Tensor, mode="rtn", seed: int = 0, offset: int = 0,
                  out: QTensor | None = None, block: int = 32) -> QTensor:
     """2D-block FP4 quantization of ``x`` (any 2-D view) into both layouts."""
@@ -153,6 +171,7 @@ def q2d_quantize(x: torch.Tensor, mode="rtn", seed: int = 0, offset: int = 0,
     R, C = x.shape
     if out is None:
         out = QTensor(FP4_2D, R, C, x.device, block)
+    _same_device(x.device, out)
     _check(_lib.q2d_quantize(x.data_ptr(), _dtype_code(x.dtype), R, C, x.stride(0), x.stride(1),
                              block, _ROUND[mode], int(seed), int(offset), out.ptr(),
                              _stream(x.device)), "q2d_quantize")
@@ -166,6 +185,7 @@ def q2d_quantize_1d(x: torch.Tensor, mode="rtn", seed: int = 0, offset: int = 0,
     R, C = x.shape
     if out is None:
         out = QTensor(FP4_1D, R, C, x.device, block)
+    _same_device(x.device, out)
     _check(_lib.q2d_quantize_1d(x.data_ptr(), _dtype_code(x.dtype), R, C, x.stride(0), x.stride(1),
                                 block, _ROUND[mode], int(seed), int(offset), out.ptr(),
                                 _stream(x.device)), "q2d_quantize_1d")
@@ -178,6 +198,7 @@ def mxfp8_quantize(x: torch.Tensor, out: QTensor | None = None) -> QTensor:
     R, C = x.shape
     if out is None:
         out = QTensor(MXFP8, R, C, x.device)
+    _same_device(x.device, out)
     _check(_lib.mxfp8_quantize(x.data_ptr(), _dtype_code(x.dtype), R, C, x.stride(0), x.stride(1),
                                out.ptr(), _stream(x.device)), "mxfp8_quantize")
     return out
@@ -195,6 +216,7 @@ def q2d_dequantize(q: QTensor, copy: int = 0, out_dtype=torch.float32, exps: boo
     if out.dim() != 2 or out.stride(1) != 1 or tuple(out.shape) != (R, C):
         raise Q2DError("output must be a row-major R x C tensor")
     e = torch.empty((R, C), dtype=torch.int8, device=q.device) if exps else None
+    _same_device(q.device, out, e)
     _check(_lib.q2d_dequantize(q.ptr(), int(copy), out.data_ptr(), _dtype_code(out.dtype), out.stride(0),
                                e.data_ptr() if e is not None else None, C, _stream(q.device)),
            "q2d_dequantize")
@@ -210,6 +232,7 @@ def q2d_gemm(A: QTensor, transA: int, B: QTensor, transB: int, out: torch.Tensor
         out = torch.empty((M, N), dtype=out_dtype, device=A.device)
     if out.dim() != 2 or out.stride(1) != 1:
         raise Q2DError("output must be a row-major 2-D tensor")
+    _same_device(A.device, B, out)
     _check(_lib.q2d_gemm(A.ptr(), int(transA), B.ptr(), int(transB), out.data_ptr(),
                          _dtype_code(out.dtype), out.stride(0), int(bool(accumulate)),
                          _stream(A.device)), "q2d_gemm")
@@ -224,6 +247,7 @@ def q2d_gemm_quantized(A: QTensor, transA: int, B: QTensor, transB: int, mode="r
     N = B.cols if transB else B.rows
     if out is None:
         out = QTensor(FP4_2D, M, N, A.device)
+    _same_device(A.device, B, out)
     _check(_lib.q2d_gemm_quantized(A.ptr(), int(transA), B.ptr(), int(transB), _ROUND[mode], out.ptr(),
                                    _stream(A.device)), "q2d_gemm_quantized")
     return out
@@ -246,6 +270,7 @@ def q2d_linear_fwd(X: torch.Tensor, W: torch.Tensor, mode_x="rtn", mode_w="rtn",
     qW = qW or QTensor(FP4_2D, N, K, X.device, block)
     if Y is None:
         Y = torch.empty((T, N), dtype=y_dtype, device=X.device)
+    _same_device(X.device, W, qX, qW, Y)
     _check(_lib.q2d_linear_fwd(X.data_ptr(), W.data_ptr(), _dtype_code(X.dtype), T, N, K,
                                _ROUND[mode_x], _ROUND[mode_w], int(seed), int(offset_x),
                                int(offset_w), qX.ptr(), qW.ptr(), Y.data_ptr(),
@@ -270,6 +295,7 @@ def q2d_linear_bwd(dY: torch.Tensor, qX: QTensor, qW: QTensor, mode_dy="sr", see
     if dW is None:
         dW = torch.zeros((N, K), dtype=dw_dtype, device=dY.device) if accumulate_dw else \
             torch.empty((N, K), dtype=dw_dtype, device=dY.device)
+    _same_device(dY.device, qX, qW, qdY, dX, dW)
     _check(_lib.q2d_linear_bwd(dY.data_ptr(), _dtype_code(dY.dtype), qX.ptr(), qW.ptr(),
                                _ROUND[mode_dy], int(seed), int(offset_dy), qdY.ptr(),
                                dX.data_ptr(), _dtype_code(dX.dtype), dW.data_ptr(),
@@ -300,6 +326,7 @@ def q2d_grouped_quantize(x: torch.Tensor, seg_offsets: torch.Tensor, mode="rtn",
     nseg = _check_offsets(seg_offsets, x.device)
     if out is None:
         out = QTensor(FP4_2D, S, C, x.device, block, nseg=nseg)
+    _same_device(x.device, out)
     _check(_lib.q2d_grouped_quantize(x.data_ptr(), _dtype_code(x.dtype), S, C, x.stride(0), nseg,
                                      seg_offsets.data_ptr(), block, _ROUND[mode], int(seed),
                                      int(offset), out.ptr(), _stream(x.device)),
@@ -322,6 +349,7 @@ def q2d_grouped_gemm(A: QTensor, transA: int, B: QTensor, transB: int, seg_offse
         out = torch.empty(shape, dtype=out_dtype, device=A.device)
     if out.dim() != 2 or out.stride(1) != 1 or tuple(out.shape) != shape:
         raise Q2DError("output must be a row-major %s tensor" % (shape,))
+    _same_device(A.device, B, out)
     _check(_lib.q2d_grouped_gemm(A.ptr(), int(transA), B.ptr(), int(transB), nseg,
                                  seg_offsets.data_ptr(), S, out.data_ptr(), _dtype_code(out.dtype),
                                  out.stride(0), int(bool(accumulate)), _stream(A.device)),

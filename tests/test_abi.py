@@ -257,3 +257,18 @@ def test_grouped_error_paths(q2d):
     assert L.q2d_tensor_init(ctypes.byref(m), 1, 4 * 96, 64, 32, sizes) == 0
     m.codes, m.scales = fake, fake
     assert G(A, 0, ctypes.byref(m), 0, 4, fake, 300, fake, 0, 96, 0, None) == 2   # MXFP8
+
+
+def test_binding_refuses_host_buffers(q2d):
+    """Host tensors never reach a kernel: descriptors and outputs must be on the GPU
+    (checked before any launch, so this runs without one)."""
+    import torch
+    cpu_q = q2d.QTensor(q2d.FP4_2D, 64, 96, "cpu")
+    with pytest.raises(q2d.Q2DError):
+        q2d.q2d_gemm(cpu_q, 0, cpu_q, 1)
+    with pytest.raises(q2d.Q2DError):
+        q2d.q2d_gemm_quantized(cpu_q, 0, cpu_q, 1)
+    with pytest.raises(q2d.Q2DError):
+        q2d.q2d_dequantize(cpu_q, 0)
+    with pytest.raises(q2d.Q2DError):
+        q2d.q2d_quantize(torch.zeros(64, 96))
