@@ -14,6 +14,15 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 __device__ __forceinline__ float bits_f(uint32_t u) { return __uint_as_float(u); }
 __device__ __forceinline__ uint32_t f_bits(float f) { return __float_as_uint(f); }
 
+// a ^ b ^ k in one v_bitop3_b32 (truth table 0x96, symmetric in its inputs);
+// k is wave-uniform
+__device__ __forceinline__ uint32_t xor3_uniform(uint32_t a, uint32_t b, uint32_t k)
+{
+    uint32_t r;
+    asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "s"(k));
+    return r;
+}
+
 // Philox4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC 2011): two 32x32->64
 // multiplies per round, key bumped by the Weyl constants between rounds.  The
 // key is wave-uniform, so the bumps stay scalar.
@@ -25,8 +34,8 @@ __device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t
         if (r) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
         const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
         const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
-        const uint32_t n0 = hi1 ^ c1 ^ k0;
-        const uint32_t n2 = hi0 ^ c3 ^ k1;
+        const uint32_t n0 = xor3_uniform(hi1, c1, k0);
+        const uint32_t n2 = xor3_uniform(hi0, c3, k1);
         c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
     }
     out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;

@@ -100,7 +100,8 @@ __device__ __forceinline__ uint32_t sr_pair(int sel, f2v v, uint32_t seed, float
     }
 }
 
-// Philox4x32-10 block with one 32x32->64 multiply per product (v_mad_u64_u32).
+// Philox4x32-10 block with one 32x32->64 multiply per product (v_mad_u64_u32)
+// and one three-input xor per output word.
 __device__ __forceinline__ void philox_block(uint64_t g, uint32_t o0, uint32_t o1, uint32_t k0, uint32_t k1,
                                              uint32_t w[4])
 {
@@ -110,8 +111,8 @@ __device__ __forceinline__ void philox_block(uint64_t g, uint32_t o0, uint32_t o
         if (r) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
         const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
         const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
-        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
-        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        const uint32_t n0 = xor3_uniform((uint32_t)(p1 >> 32), c1, k0);
+        const uint32_t n2 = xor3_uniform((uint32_t)(p0 >> 32), c3, k1);
         c0 = n0; c1 = (uint32_t)p1; c2 = n2; c3 = (uint32_t)p0;
     }
     w[0] = c0; w[1] = c1; w[2] = c2; w[3] = c3;
