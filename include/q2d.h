@@ -29,7 +29,10 @@
  *     is valid in stream order.  No call blocks the host.
  *   - Errors: argument errors are detected on the host before any launch and
  *     returned as a status; nothing is printed, no exception crosses the ABI.
- *     A failed launch returns Q2D_ELAUNCH.  Data-dependent conditions are not
+ *     A failed launch returns Q2D_ELAUNCH.  Extents (rows, cols, total rows)
+ *     above 2^31, and a strided view whose last storage index
+ *     (rows-1)*stride_r + (cols-1)*stride_c reaches 2^47 elements, return
+ *     Q2D_EUNSUPPORTED.  Data-dependent conditions are not
  *     errors: a block holding a NaN or an infinity gets scale byte 0xFF (the
  *     E8M0 NaN) and all-zero codes.
  *   - Thread safety: the library keeps no mutable state.
@@ -44,16 +47,26 @@
 extern "C" {
 #endif
 
-typedef enum {
+/* In C++ the enumerations get int as their fixed underlying type, so that any
+ * int a C caller passes is a value of the type (and is rejected by the argument
+ * checks) rather than undefined behaviour; the size and calling convention are
+ * those of int in both languages. */
+#ifdef __cplusplus
+#define Q2D_ENUM_BASE : int
+#else
+#define Q2D_ENUM_BASE
+#endif
+
+typedef enum Q2D_ENUM_BASE {
     Q2D_OK = 0,
     Q2D_EINVAL = 1,          /* bad argument: null pointer, size, stride, alignment, shape mismatch */
     Q2D_EUNSUPPORTED = 2,    /* valid request this build does not implement (e.g. block 16) */
     Q2D_ELAUNCH = 3          /* the HIP runtime rejected a kernel launch */
 } q2d_status;
 
-typedef enum { Q2D_F32 = 0, Q2D_BF16 = 1 } q2d_dtype;
+typedef enum Q2D_ENUM_BASE { Q2D_F32 = 0, Q2D_BF16 = 1 } q2d_dtype;
 
-typedef enum {
+typedef enum Q2D_ENUM_BASE {
     Q2D_RTN = 0,             /* round to nearest, ties to the even E2M1 code (App. E, forward) */
     Q2D_SR = 1,              /* stochastic rounding, Philox4x32-10, 16 bits per element (App. E) */
     /* Flag OR-ed into Q2D_RTN or Q2D_SR for 2D-block FP4 (q2d_quantize,
@@ -67,7 +80,7 @@ typedef enum {
     Q2D_FLOOR_SCALE = 0x10
 } q2d_round;
 
-typedef enum {
+typedef enum Q2D_ENUM_BASE {
     Q2D_FMT_FP4_2D = 0,      /* E2M1 codes, one E8M0 scale per 32x32 block (Sec. 3) */
     Q2D_FMT_MXFP8 = 1,       /* E4M3 codes, one E8M0 scale per 1x32 block (Sec. 3.2) */
     Q2D_FMT_FP4_1D = 2       /* E2M1 codes, one E8M0 scale per 1x32 block: activations

@@ -112,11 +112,31 @@ int64_t grouped_capacity(int64_t rows, int32_t nseg) { return rup(rows + 127 * (
 
 constexpr int32_t kMaxGroups = 1024;
 
+// Matrix extents: positive, and at most 2^31 per dimension, which keeps every
+// layout product and padded size far from int64 overflow.
+constexpr int64_t kMaxDim = int64_t(1) << 31;
+
+q2d_status check_dims(int64_t R, int64_t C)
+{
+    if (R <= 0 || C <= 0) return Q2D_EINVAL;
+    if (R > kMaxDim || C > kMaxDim) return Q2D_EUNSUPPORTED;
+    return Q2D_OK;
+}
+
+// The largest storage index a strided view reaches, (R-1) sr + (C-1) sc, must
+// stay below 2^47 elements (the kernels form it in 64-bit arithmetic).
+constexpr int64_t kMaxIndex = int64_t(1) << 47;
+
 q2d_status check_input(const void *x, q2d_dtype dt, int64_t R, int64_t C, int64_t sr, int64_t sc)
 {
-    if (!x || !valid_dtype(dt) || R <= 0 || C <= 0 || sr <= 0 || sc <= 0) return Q2D_EINVAL;
+    if (!x || !valid_dtype(dt) || sr <= 0 || sc <= 0) return Q2D_EINVAL;
+    q2d_status s = check_dims(R, C);
+    if (s != Q2D_OK) return s;
     if (!aligned(x, (uintptr_t)dtype_bytes(dt))) return Q2D_EINVAL;
-    if (R > (int64_t(1) << 31) || C > (int64_t(1) << 31)) return Q2D_EUNSUPPORTED;
+    int64_t a, b, last;
+    if (__builtin_mul_overflow(R - 1, sr, &a) || __builtin_mul_overflow(C - 1, sc, &b) ||
+        __builtin_add_overflow(a, b, &last) || last >= kMaxIndex)
+        return Q2D_EUNSUPPORTED;
     return Q2D_OK;
 }
 
@@ -127,7 +147,9 @@ extern "C" {
 q2d_status q2d_tensor_init(q2d_tensor *t, q2d_fmt fmt, int64_t rows, int64_t cols, int32_t block,
                            int64_t bytes[4])
 {
-    if (!t || rows <= 0 || cols <= 0) return Q2D_EINVAL;
+    if (!t) return Q2D_EINVAL;
+    const q2d_status s = check_dims(rows, cols);
+    if (s != Q2D_OK) return s;
     if (fmt != Q2D_FMT_FP4_2D && fmt != Q2D_FMT_MXFP8 && fmt != Q2D_FMT_FP4_1D) return Q2D_EINVAL;
     // 64 x 64 blocks keep the 32-granular scale grid (each block's byte in its
     // four entries), so every GEMM reads them unchanged
@@ -222,7 +244,9 @@ static q2d_status gemm_operands(const q2d_tensor *A, int transA, const q2d_tenso
         return t->block == 32 || (t->block == 64 && t->fmt == Q2D_FMT_FP4_2D);
     };
     if (!block_ok(A) || !block_ok(B)) return Q2D_EUNSUPPORTED;
-    if (A->rows <= 0 || A->cols <= 0 || B->rows <= 0 || B->cols <= 0) return Q2D_EINVAL;
+    q2d_status s = check_dims(A->rows, A->cols);
+    if (s == Q2D_OK) s = check_dims(B->rows, B->cols);
+    if (s != Q2D_OK) return s;
     const int64_t M = transA ? A->cols : A->rows, Ka = transA ? A->rows : A->cols;
     const int64_t N = transB ? B->cols : B->rows, Kb = transB ? B->rows : B->cols;
     if (Ka != Kb) return Q2D_EINVAL;
@@ -331,7 +355,9 @@ q2d_status q2d_linear_bwd(const void *dY, q2d_dtype dt, const q2d_tensor *qX, co
 q2d_status q2d_grouped_tensor_init(q2d_tensor *t, int64_t rows, int64_t cols, int32_t nseg, int32_t block,
                                    int64_t bytes[4])
 {
-    if (nseg <= 0 || nseg > kMaxGroups || rows <= 0) return Q2D_EINVAL;
+    if (nseg <= 0 || nseg > kMaxGroups) return Q2D_EINVAL;
+    const q2d_status s = check_dims(rows, cols);
+    if (s != Q2D_OK) return s;
     if (block != 32) return Q2D_EUNSUPPORTED;
     return q2d_tensor_init(t, Q2D_FMT_FP4_2D, grouped_capacity(rows, nseg), cols, block, bytes);
 }
@@ -372,6 +398,10 @@ q2d_status q2d_grouped_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B
     if (A->fmt != Q2D_FMT_FP4_2D || B->fmt != Q2D_FMT_FP4_2D) return Q2D_EUNSUPPORTED;
     if (A->block != 32 || B->block != 32) return Q2D_EUNSUPPORTED;
     if (!aligned(C, (uintptr_t)dtype_bytes(c_dt))) return Q2D_EINVAL;
+    q2d_status s = check_dims(A->rows, A->cols);
+    if (s == Q2D_OK) s = check_dims(B->rows, B->cols);
+    if (s == Q2D_OK && total_rows > kMaxDim) s = Q2D_EUNSUPPORTED;
+    if (s != Q2D_OK) return s;
     const int64_t cap = grouped_capacity(total_rows, nseg);
     const Layout la = layout_of(Q2D_FMT_FP4_2D, A->rows, A->cols), lb = layout_of(Q2D_FMT_FP4_2D, B->rows, B->cols);
     GemmArgs g = {};
@@ -441,7 +471,9 @@ q2d_status q2d_dequantize(const q2d_tensor *t, int copy, void *out, q2d_dtype ou
     if (!t || !out || (copy != 0 && copy != 1) || !valid_dtype(out_dt)) return Q2D_EINVAL;
     if (t->fmt != Q2D_FMT_FP4_2D && t->fmt != Q2D_FMT_MXFP8 && t->fmt != Q2D_FMT_FP4_1D) return Q2D_EINVAL;
     if (t->block != 32 && !(t->block == 64 && t->fmt == Q2D_FMT_FP4_2D)) return Q2D_EUNSUPPORTED;
-    if (t->rows <= 0 || t->cols <= 0 || ldo < t->cols || (exps && lde < t->cols)) return Q2D_EINVAL;
+    const q2d_status s = check_dims(t->rows, t->cols);
+    if (s != Q2D_OK) return s;
+    if (ldo < t->cols || (exps && lde < t->cols)) return Q2D_EINVAL;
     const Layout l = layout_of((q2d_fmt)t->fmt, t->rows, t->cols);
     const uint8_t *codes = copy ? t->codes_t : t->codes;
     const uint8_t *scales = copy ? t->scales_t : t->scales;

@@ -58,6 +58,11 @@ def test_error_paths(q2d):
     assert L.q2d_tensor_init(ctypes.byref(d), 0, 5, 5, 16, sizes) == 2
     assert L.q2d_tensor_init(ctypes.byref(d), 7, 5, 5, 32, sizes) == 1
     assert L.q2d_tensor_init(None, 0, 5, 5, 32, sizes) == 1
+    # extents beyond 2^31 (their layout products would overflow int64) are unsupported
+    for huge in (2 ** 31 + 1, 2 ** 62, 2 ** 63 - 1):
+        assert L.q2d_tensor_init(ctypes.byref(d), 0, huge, 64, 32, sizes) == 2
+        assert L.q2d_tensor_init(ctypes.byref(d), 2, 64, huge, 32, sizes) == 2
+        assert L.q2d_grouped_tensor_init(ctypes.byref(d), huge, 64, 4, 32, sizes) == 2
     assert L.q2d_tensor_init(ctypes.byref(d), 0, 64, 64, 32, sizes) == 0
     fake = 0x1000
     # no buffers attached
