@@ -96,6 +96,30 @@ def test_gemm_fp4_multi_tile_per_workgroup(q2d, M, N, K, ta, tb):
     check_bf16(c16, ref + c0.float().cpu().numpy().astype(np.float64))
 
 
+def test_gemm_deterministic(q2d):
+    """Two runs of each persistent-kernel GEMM (forward with bf16 output, weight
+    gradient with fp32 output, the quantizing epilogue) on the same operands give
+    identical bytes: no atomics, a fixed reduction order per output element."""
+    T, N, K = 2048, 4096, 1024                      # 128 output tiles of 256 x 256
+    X = synth.normal((T, K), 1.0, 611, torch.bfloat16, device=DEV)
+    W = synth.normal((N, K), 0.02, 612, torch.bfloat16, device=DEV)
+    dY = synth.normal((T, N), 1e-3, 613, torch.bfloat16, device=DEV)
+    qx, qw, qdy = q2d.q2d_quantize(X, "sr", 1, 0), q2d.q2d_quantize(W, "sr", 1, 1), q2d.q2d_quantize(dY, "sr", 1, 2)
+    runs = []
+    for _ in range(2):
+        y = torch.full((T, N), float("nan"), dtype=torch.bfloat16, device=DEV)
+        dw = torch.full((N, K), float("nan"), dtype=torch.float32, device=DEV)
+        q2d.q2d_gemm(qx, 0, qw, 0, out=y)
+        q2d.q2d_gemm(qdy, 1, qx, 1, out=dw)
+        qy = q2d.q2d_gemm_quantized(qx, 0, qw, 0, "rtn")
+        torch.cuda.synchronize()
+        runs.append([y.view(torch.int16).clone(), dw.view(torch.int32).clone(), qy.codes.clone(),
+                     qy.codes_t.clone(), qy.scales.clone(), qy.scales_t.clone()])
+    for a, b in zip(*runs):
+        assert torch.equal(a, b)
+    assert not torch.isnan(runs[0][0].view(torch.bfloat16)).any()
+
+
 def test_gemm_accumulate_and_ldc(q2d):
     A = synth.normal((200, 320), 1.0, 1, torch.bfloat16, device=DEV)
     B = synth.normal((150, 320), 1.0, 2, torch.bfloat16, device=DEV)

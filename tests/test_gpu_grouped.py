@@ -5,6 +5,8 @@ orientations) equals ``oracle.quantize_fp4_grouped`` of the same input, for
 RTN and SR, bf16 and fp32, dense and row-strided inputs; segment lengths
 cover empty experts, single rows, lengths around the 32-row block and the
 128-row padding, and several 256-row GEMM tiles; the maximum of 1024 experts.
+Each padded segment also equals an ungrouped quantization of that expert's
+rows (device against device).
 
 GEMMs: per expert, relative Frobenius error <= 1e-5 (fp32 output) of the
 device result against float64 products of the oracle's operands; bf16
@@ -73,6 +75,34 @@ def quant_grouped(q2d, x, off, mode, seed=0, offset=0, x_cpu=None):
 
 
 # ------------------------------------------------------------------ quantizer
+
+@pytest.mark.parametrize("counts", ["edges", "sparse"])
+@pytest.mark.parametrize("C", [200, 384])
+def test_grouped_equals_per_expert_calls(q2d, counts, C):
+    """Each padded segment of a grouped RTN quantization holds exactly what an
+    ungrouped q2d_quantize of that expert's rows writes (GPU against GPU):
+    segments are quantized as matrices of their own, from row 0 of the segment."""
+    cnt = COUNTS[counts]
+    off = np.concatenate([[0], np.cumsum(cnt)]).astype(np.int64)
+    S = max(int(off[-1]), 1)
+    x = synth.normal((S, C), 1.0, 4242 + C, torch.bfloat16, device=DEV)
+    q = q2d.q2d_grouped_quantize(x, dev_offsets(off), "rtn")
+    P = 0
+    for e, n in enumerate(cnt):
+        if n:
+            u = q2d.q2d_quantize(x[off[e]:off[e] + n], "rtn")
+            np_ = -(-n // 128) * 128
+            torch.cuda.synchronize()
+            got = {"codes": q.codes[P:P + n], "scales": q.scales[P // 32:P // 32 + -(-n // 32)],
+                   "codes_t": q.codes_t[:, P // 2:P // 2 + np_ // 2],
+                   "scales_t": q.scales_t[:, P // 32:P // 32 + np_ // 32]}
+            want = {"codes": u.codes[:n], "scales": u.scales[:-(-n // 32)],
+                    "codes_t": u.codes_t[:, :np_ // 2], "scales_t": u.scales_t[:, :np_ // 32]}
+            for k in BUFS:
+                assert torch.equal(got[k], want[k]), (counts, C, e, n, k)
+            P += np_
+
+
 
 @pytest.mark.parametrize("counts", list(COUNTS))
 @pytest.mark.parametrize("C", [96, 200, 384])
