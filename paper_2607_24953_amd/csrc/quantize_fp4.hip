@@ -495,8 +495,12 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
 // Vector-load stochastic-rounding variants at most 168 VGPRs (three waves per
 // SIMD): they are bound by their Philox arithmetic and need the occupancy to
 // hide its latency (the grouped one would otherwise take 169 and drop to two).
+// Dense vector-load round-to-nearest variants at most 128 (four waves per SIMD,
+// two 8-wave workgroups per CU instead of one): 3-5 % more bandwidth despite a
+// few spilled registers.
 template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED, int WC, bool ONED>
-__global__ __launch_bounds__(256 * WC) __attribute__((amdgpu_waves_per_eu(VEC && SR ? 3 : 1))) void fp4_quantize_kernel(QuantArgs a)
+__global__ __launch_bounds__(256 * WC)
+__attribute__((amdgpu_waves_per_eu(VEC && SR ? 3 : (VEC && !GROUPED ? 4 : 1)))) void fp4_quantize_kernel(QuantArgs a)
 {
     static_assert(!(ONED && GROUPED), "grouped tensors use 2D blocks");
     constexpr int kTC = 128 * WC;
