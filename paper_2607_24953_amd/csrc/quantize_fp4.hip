@@ -139,7 +139,6 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
     const int rg = lane >> 4, cc = lane & 15;
     const int64_t r0 = strip_r + 8 * rg;
     const int64_t c0 = tc * kTC + wc * 128 + 8 * cc;
-    const bool col_ok = tc * kTC + wc * 128 < a.cols_pad;     // strip inside the padded width
     const T *x = reinterpret_cast<const T *>(a.x);
 
     // ---- load the 8 x 8 sub-block (0 outside R x C).  bf16: v[i][k] holds
@@ -420,6 +419,12 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
     __shared__ uint8_t st_rs[ONED ? kTile : 1][4 * WC];     // 1D: row scales of the tile
     __shared__ uint8_t st_cs[ONED ? kTC : 1][4];            // 1D: column scales of the tile
     {
+        // the lane geometry again, from the thread index: cheaper than keeping it
+        // live across the conversion (the opaque copy stops the compiler from
+        // reusing the values computed at the top)
+        int t = threadIdx.x;
+        asm volatile("" : "+v"(t));
+        const int wr = (t >> 6) / WC, wc = (t >> 6) % WC, rg = (t & 63) >> 4, cc = t & 15;
         const int rl = wr * 32 + 8 * rg;
 #pragma unroll
         for (int i = 0; i < 8; ++i) st_r[rl + i][wc * 16 + cc] = rowp[i];
@@ -484,9 +489,14 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
         }
         return;
     }
-    if (col_ok && rg == 0 && (cc & 3) == 0) {
+    // the block's scale byte, from one lane per 32 x 32 block (lane geometry
+    // recomputed, as above)
+    int t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    const int tw = t >> 6, tl = t & 63;
+    if (tc * kTC + (tw % WC) * 128 < a.cols_pad && (tl >> 4) == 0 && (tl & 3) == 0) {
         const uint8_t sbyte = finite ? (uint8_t)(e + 127) : (uint8_t)0xFF;
-        const int64_t rb = strip_r >> 5, cb = c0 >> 5;
+        const int64_t rb = (tr * kTile + (tw / WC) * 32) >> 5, cb = (tc * kTC + (tw % WC) * 128 + 8 * (tl & 15)) >> 5;
         if (a.scales && rb < a.nbr) a.scales[rb * a.ld_scales + cb] = sbyte;
         if (a.scales_t && cb < a.nbc) a.scales_t[cb * a.ld_scales_t + rb] = sbyte;
     }
