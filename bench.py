@@ -40,6 +40,9 @@ WORKLOAD_TEXT = {
     "dense_7b": "7B-class dense linears fwd+bwd (QKV 4096->12288, O 4096->4096, gate/up "
                 "4096->11008, down 11008->4096), tokens 16384, bf16 inputs, 32x32 2D-block FP4 "
                 "(X, W round-to-nearest; dY stochastic), X with 1% Student-t outlier channels",
+    "tiny": "Tiny linear fwd+bwd: W 256x256 ~N(0,0.02), X 128x256 ~N(0,1), dY 128x256 ~N(0,1e-3), "
+            "float32 inputs, 32x32 2D-block FP4 with stochastic rounding (seed 0) on X, W and dY; "
+            "fwd, dX and dW GEMMs",
     "dense_1b": "1B-class dense MLP fwd+bwd (up 2048->5632, down 5632->2048), tokens 8192, "
                 "bf16 inputs, 32x32 2D-block FP4 with stochastic rounding on X, W and dY",
     "moe_30b": "30B-class MoE expert FFN fwd+bwd: 16384 tokens, top-8 of 128 experts "
@@ -90,7 +93,7 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="dense_7b", choices=sorted(WORKLOAD_TEXT))
-    p.add_argument("--also", default="moe_30b,mixed_7b,dense_7b_1d,dense_7b_b64,dense_7b_yq_fused,"
+    p.add_argument("--also", default="dense_1b,tiny,moe_30b,mixed_7b,dense_7b_1d,dense_7b_b64,dense_7b_yq_fused,"
                                      "dense_7b_yq_separate",
                    help="further workloads measured in the same run (comma list, or 'none')")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -349,6 +352,7 @@ def measure(step, torch, steps: int, warmup: int) -> dict:
         n[1] += ms; n[2] += work; n[3] += 1
     ms_per_step = wall * 1e3 / steps
     res = {"ms_per_step": ms_per_step, "value": step.flops / (ms_per_step * 1e-3) / 1e12,
+           "quant_gb_per_step": sum(o[3] for o in step.ops if o[0].startswith("quant")) / 1e9,
            "kinds": {}, "per_kernel": {},
            "launches": len(step.ops) * (warmup + 2 * steps)}      # one dispatch per op
     for kind, (ms, work, n, abytes) in kinds.items():
@@ -398,8 +402,11 @@ def cpu_baseline(w, tokens: int):
                       "%.3f TFLOP" % (len(w.linears), tokens, dt, flops / 1e12)}
 
 
-PROFILE_WORKLOADS = ("dense_7b", "moe_30b", "mixed_7b", "dense_7b_1d", "dense_7b_b64", "dense_7b_yq_fused")
+PROFILE_WORKLOADS = ("dense_7b", "dense_1b", "moe_30b", "mixed_7b", "dense_7b_1d", "dense_7b_b64",
+                     "dense_7b_yq_fused")
 PROFILE_FILES = {
+    "dense_1b": [("fp4_kernels.dense_1b.md", ("gemm_fp4", "quant_fp4"))],
+    "tiny": [("fp4_kernels.tiny.md", ("gemm_fp4", "quant_fp4"))],
     "dense_7b": [("gemm_fp4_persistent_kernel.dense_7b.md", ("gemm_fp4",)),
                  ("fp4_quantize_kernel.dense_7b.md", ("quant_fp4",))],
     "moe_30b": [("grouped_fp4_kernels.moe_30b.md", ("gemm_fp4_grouped", "gemm_fp4_grouped_k", "quant_fp4_grouped",
@@ -414,7 +421,7 @@ PROFILE_COMMANDS = """cd /tmp && export TMPDIR=/tmp; R=/root/repo; O=${PROFILE_O
 rocprofv3 --kernel-trace --stats --output-format csv -d $O/trace -o bench -- python3 $R/bench.py > $O/bench_trace.log 2>&1
 for c in FETCH_SIZE WRITE_SIZE; do
   rocprofv3 --pmc $c --output-format csv -d $O/copy_$c -o copy -- python3 $R/bench.py --copy-calibration 1073741824 > $O/copy_$c.log 2>&1
-  for wl in dense_7b moe_30b mixed_7b dense_7b_1d dense_7b_b64 dense_7b_yq_fused; do
+  for wl in dense_7b dense_1b moe_30b mixed_7b dense_7b_1d dense_7b_b64 dense_7b_yq_fused; do
     rocprofv3 --pmc $c --output-format csv -d $O/${wl}_$c -o $wl -- python3 $R/bench.py --workload $wl --also none --steps 1 --warmup 0 --no-cpu-baseline > $O/${wl}_$c.log 2>&1
   done
 done
@@ -659,6 +666,7 @@ def main():
         "config": {"workload": WORKLOAD_TEXT[args.workload], "name": args.workload,
                    "gemms_per_step": sum(1 for o in step.ops if o[0].startswith("gemm")),
                    "gemm_tflop_per_step": step.flops / 1e12,
+                   "quantizer_gb_per_step": round(res["quant_gb_per_step"], 6),
                    "quantizations_per_step": sum(1 for o in step.ops if o[0].startswith("quant")),
                    "block": w.block},
         "roofline": roof,
@@ -682,6 +690,7 @@ def main():
             rec["other_workloads"][name] = {
                 "workload": WORKLOAD_TEXT[name], "TFLOP/s": round(ro["value"], 2),
                 "ms_per_step": round(ro["ms_per_step"], 4), "gemm_tflop_per_step": so.flops / 1e12,
+                "quantizer_gb_per_step": round(ro["quant_gb_per_step"], 6),
                 "kinds": ro["kinds"], "per_kernel": ro["per_kernel"], "launches": ro["launches"]}
             del so, wo
             torch.cuda.empty_cache()

@@ -318,11 +318,17 @@ q2d_status q2d_dequantize(const q2d_tensor *t, int copy, void *out, q2d_dtype ou
  * (rows counted from x), so a grouped call draws the same bits as quantizing
  * each segment's view of the same buffer.
  *
+ * The offsets are read on the device, where they cannot be checked before a
+ * launch.  The kernels use o'[i] = min(max(0, seg_offsets[0..i]), rows) (rows
+ * = total_rows for the GEMM): a valid table is unchanged, and any other one
+ * cannot take a kernel outside x, C or the grouped capacity; its results are
+ * those of the table o'.
+ *
  * q2d_grouped_tensor_init: layout of the padded form (rows = the capacity
  * roundup(rows + 127 * nseg, 128), cols as given); bytes[] as q2d_tensor_init.
  * Rows beyond the last segment's padded end are not written.  Q2D_EINVAL for
  * rows or cols <= 0 or nseg outside [1, 1024]; Q2D_EUNSUPPORTED for a block
- * other than 32.
+ * other than 32 or a capacity above 2^31 - 1 rows.
  */
 q2d_status q2d_grouped_tensor_init(q2d_tensor *t, int64_t rows, int64_t cols, int32_t nseg,
                                    int32_t block, int64_t bytes[4]);

@@ -12,7 +12,11 @@ GEMMs run on quantized operands through ``q2d_linear_fwd`` / ``q2d_linear_bwd``:
   the gradients above are returned for x and W as they are.
 
 Each call draws fresh stochastic-rounding streams: the layer's seed with
-offsets 3n, 3n+1, 3n+2 for X, W and dY of its n-th forward call.  The weight
+offsets 3n, 3n+1, 3n+2 for X, W and dY of its n-th forward call.  A layer built
+without a seed takes the next value of a process-wide counter, so the layers of
+a model draw independent streams (App. E asks for unbiased, independent
+rounding; one seed shared by every layer would give the n-th gradients of all
+layers the same random bits at the same storage indices).  The weight
 (the master copy, usually float32) is cast to the input's dtype (float32 or
 bfloat16) before quantization; Y and dX have the input's dtype, dW is computed
 in float32 and cast to the weight's dtype.
@@ -24,6 +28,7 @@ blocks (App. C, "Activations"); ``block=64`` uses 64 x 64 blocks (Table 4).
 """
 from __future__ import annotations
 
+import itertools
 import math
 
 import torch
@@ -64,15 +69,21 @@ class _Q2DLinearFunction(torch.autograd.Function):
         return dX.reshape(ctx.x_shape).to(ctx.x_dtype), dW.to(ctx.w_dtype), None
 
 
+# seeds of layers built without one (distinct per layer within a process)
+_SEEDS = itertools.count(0x5EED0001)
+
+
 class Q2DLinear(torch.nn.Module):
     """Bias-free linear layer on 2D-block FP4 GEMMs (see the module docstring)."""
 
     def __init__(self, in_features: int, out_features: int, *, mode_x: str = "rtn", mode_w: str = "rtn",
-                 mode_dy: str = "sr", activations: str = "2d", block: int = 32, seed: int = 0,
+                 mode_dy: str = "sr", activations: str = "2d", block: int = 32, seed: int | None = None,
                  device=None, dtype=torch.float32):
         super().__init__()
         if activations not in ("2d", "1d"):
             raise ValueError("activations must be '2d' or '1d'")
+        if seed is None:
+            seed = next(_SEEDS)
         self.in_features, self.out_features = in_features, out_features
         self.mode_x, self.mode_w, self.mode_dy = mode_x, mode_w, mode_dy
         self.activations, self.block, self.seed = activations, block, seed
@@ -87,6 +98,6 @@ class Q2DLinear(torch.nn.Module):
         return _Q2DLinearFunction.apply(x, self.weight, self)
 
     def extra_repr(self) -> str:
-        return "in=%d, out=%d, x=%s, w=%s, dy=%s, activations=%s, block=%d" % (
+        return "in=%d, out=%d, x=%s, w=%s, dy=%s, activations=%s, block=%d, seed=%#x" % (
             self.in_features, self.out_features, self.mode_x, self.mode_w, self.mode_dy,
-            self.activations, self.block)
+            self.activations, self.block, self.seed)

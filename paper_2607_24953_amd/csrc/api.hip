@@ -3,6 +3,7 @@
 #include "q2d.h"
 #include "kernels.hpp"
 
+#include <initializer_list>
 #include <stdint.h>
 
 namespace {
@@ -110,6 +111,9 @@ QuantArgs make_quant_args(const void *x, int64_t R, int64_t C, int64_t sr, int64
 // boundary, so sum_e roundup(n_e, 128) <= rows + 127 * nseg.
 int64_t grouped_capacity(int64_t rows, int32_t nseg) { return rup(rows + 127 * (int64_t)nseg, 128); }
 
+// The kernels hold segment offsets and padded row starts in 32-bit integers.
+constexpr int64_t kMaxGroupedRows = INT32_MAX;
+
 constexpr int32_t kMaxGroups = 1024;
 
 // Matrix extents: positive, and at most 2^31 per dimension, which keeps every
@@ -168,9 +172,12 @@ q2d_status q2d_tensor_init(q2d_tensor *t, q2d_fmt fmt, int64_t rows, int64_t col
     return Q2D_OK;
 }
 
-q2d_status q2d_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols, int64_t stride_r,
-                        int64_t stride_c, int32_t block, q2d_round mode, uint64_t seed,
-                        uint64_t offset, q2d_tensor *out, hipStream_t stream)
+// The entry points below check every argument before they launch; with
+// go == false they only check (the composite linear-layer calls check all of
+// their steps before the first launch).
+static q2d_status quantize_impl(const void *x, q2d_dtype dt, int64_t rows, int64_t cols, int64_t stride_r,
+                                int64_t stride_c, int32_t block, q2d_round mode, uint64_t seed, uint64_t offset,
+                                q2d_tensor *out, hipStream_t stream, bool go)
 {
     q2d_status s = check_input(x, dt, rows, cols, stride_r, stride_c);
     if (s != Q2D_OK) return s;
@@ -183,13 +190,21 @@ q2d_status q2d_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols,
     QuantArgs a = make_quant_args(x, rows, cols, stride_r, stride_c, seed, offset, out);
     a.block = block;
     a.floor_scale = ((int)mode & Q2D_FLOOR_SCALE) != 0;
-    if (launch_fp4_quantize(a, dtype_bytes(dt), rmode == Q2D_SR, false, stream) != hipSuccess) return Q2D_ELAUNCH;
+    if (go && launch_fp4_quantize(a, dtype_bytes(dt), rmode == Q2D_SR, false, stream) != hipSuccess)
+        return Q2D_ELAUNCH;
     return Q2D_OK;
 }
 
-q2d_status q2d_quantize_1d(const void *x, q2d_dtype dt, int64_t rows, int64_t cols, int64_t stride_r,
-                           int64_t stride_c, int32_t block, q2d_round mode, uint64_t seed, uint64_t offset,
-                           q2d_tensor *out, hipStream_t stream)
+q2d_status q2d_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols, int64_t stride_r,
+                        int64_t stride_c, int32_t block, q2d_round mode, uint64_t seed,
+                        uint64_t offset, q2d_tensor *out, hipStream_t stream)
+{
+    return quantize_impl(x, dt, rows, cols, stride_r, stride_c, block, mode, seed, offset, out, stream, true);
+}
+
+static q2d_status quantize_1d_impl(const void *x, q2d_dtype dt, int64_t rows, int64_t cols, int64_t stride_r,
+                                   int64_t stride_c, int32_t block, q2d_round mode, uint64_t seed, uint64_t offset,
+                                   q2d_tensor *out, hipStream_t stream, bool go)
 {
     q2d_status s = check_input(x, dt, rows, cols, stride_r, stride_c);
     if (s != Q2D_OK) return s;
@@ -202,8 +217,16 @@ q2d_status q2d_quantize_1d(const void *x, q2d_dtype dt, int64_t rows, int64_t co
     // a transposed view's rowwise blocks are its storage's column blocks: the
     // swap of make_quant_args sends each copy to the right buffers
     const QuantArgs a = make_quant_args(x, rows, cols, stride_r, stride_c, seed, offset, out);
-    if (launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, true, stream) != hipSuccess) return Q2D_ELAUNCH;
+    if (go && launch_fp4_quantize(a, dtype_bytes(dt), mode == Q2D_SR, true, stream) != hipSuccess)
+        return Q2D_ELAUNCH;
     return Q2D_OK;
+}
+
+q2d_status q2d_quantize_1d(const void *x, q2d_dtype dt, int64_t rows, int64_t cols, int64_t stride_r,
+                           int64_t stride_c, int32_t block, q2d_round mode, uint64_t seed, uint64_t offset,
+                           q2d_tensor *out, hipStream_t stream)
+{
+    return quantize_1d_impl(x, dt, rows, cols, stride_r, stride_c, block, mode, seed, offset, out, stream, true);
 }
 
 q2d_status mxfp8_quantize(const void *x, q2d_dtype dt, int64_t rows, int64_t cols, int64_t stride_r,
@@ -279,8 +302,8 @@ static q2d_status gemm_operands(const q2d_tensor *A, int transA, const q2d_tenso
     return Q2D_OK;
 }
 
-q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, void *C,
-                    q2d_dtype c_dt, int64_t ldc, int accumulate, hipStream_t stream)
+static q2d_status gemm_impl(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, void *C,
+                            q2d_dtype c_dt, int64_t ldc, int accumulate, hipStream_t stream, bool go)
 {
     if (!A || !B || !C || !valid_dtype(c_dt)) return Q2D_EINVAL;
     if (accumulate != 0 && accumulate != 1) return Q2D_EINVAL;
@@ -292,9 +315,15 @@ q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int tr
     if (!aligned(C, (uintptr_t)dtype_bytes(c_dt))) return Q2D_EINVAL;
     g.c = C; g.ldc = ldc;
     g.accumulate = accumulate;
-    if (launch_gemm(g, fp4 ? kFmtFp4Block2D : kFmtMxfp8, c_dt == Q2D_BF16, stream) != hipSuccess)
+    if (go && launch_gemm(g, fp4 ? kFmtFp4Block2D : kFmtMxfp8, c_dt == Q2D_BF16, stream) != hipSuccess)
         return Q2D_ELAUNCH;
     return Q2D_OK;
+}
+
+q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, void *C,
+                    q2d_dtype c_dt, int64_t ldc, int accumulate, hipStream_t stream)
+{
+    return gemm_impl(A, transA, B, transB, C, c_dt, ldc, accumulate, stream, true);
 }
 
 q2d_status q2d_gemm_quantized(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, q2d_round mode,
@@ -328,13 +357,16 @@ q2d_status q2d_linear_fwd(const void *X, const void *W, q2d_dtype dt, int64_t T,
                           hipStream_t stream)
 {
     if (!qX || !qW || !qX->codes || !qW->codes) return Q2D_EINVAL;
-    q2d_status s = qX->fmt == Q2D_FMT_FP4_1D
-                       ? q2d_quantize_1d(X, dt, T, K, K, 1, 32, mode_x, seed, offset_x, qX, stream)
-                       : q2d_quantize(X, dt, T, K, K, 1, qX->block, mode_x, seed, offset_x, qX, stream);
-    if (s != Q2D_OK) return s;
-    s = q2d_quantize(W, dt, N, K, K, 1, qW->block, mode_w, seed, offset_w, qW, stream);
-    if (s != Q2D_OK) return s;
-    return q2d_gemm(qX, 0, qW, 0, Y, y_dt, N, 0, stream);
+    // every step is checked (go = false) before the first one is launched
+    for (const bool go : {false, true}) {
+        q2d_status s = qX->fmt == Q2D_FMT_FP4_1D
+                           ? quantize_1d_impl(X, dt, T, K, K, 1, 32, mode_x, seed, offset_x, qX, stream, go)
+                           : quantize_impl(X, dt, T, K, K, 1, qX->block, mode_x, seed, offset_x, qX, stream, go);
+        if (s == Q2D_OK) s = quantize_impl(W, dt, N, K, K, 1, qW->block, mode_w, seed, offset_w, qW, stream, go);
+        if (s == Q2D_OK) s = gemm_impl(qX, 0, qW, 0, Y, y_dt, N, 0, stream, go);
+        if (s != Q2D_OK) return s;
+    }
+    return Q2D_OK;
 }
 
 q2d_status q2d_linear_bwd(const void *dY, q2d_dtype dt, const q2d_tensor *qX, const q2d_tensor *qW,
@@ -345,11 +377,13 @@ q2d_status q2d_linear_bwd(const void *dY, q2d_dtype dt, const q2d_tensor *qX, co
     const int64_t T = qX->rows, K = qX->cols, N = qW->rows;
     if (qW->cols != K || qdY->rows != T || qdY->cols != N) return Q2D_EINVAL;
     if (!qdY->codes || !qdY->codes_t || !qX->codes_t || !qW->codes_t) return Q2D_EINVAL;
-    q2d_status s = q2d_quantize(dY, dt, T, N, N, 1, qdY->block, mode_dy, seed, offset_dy, qdY, stream);
-    if (s != Q2D_OK) return s;
-    s = q2d_gemm(qdY, 0, qW, 1, dX, dx_dt, K, 0, stream);
-    if (s != Q2D_OK) return s;
-    return q2d_gemm(qdY, 1, qX, 1, dW, dw_dt, K, accumulate_dw, stream);
+    for (const bool go : {false, true}) {
+        q2d_status s = quantize_impl(dY, dt, T, N, N, 1, qdY->block, mode_dy, seed, offset_dy, qdY, stream, go);
+        if (s == Q2D_OK) s = gemm_impl(qdY, 0, qW, 1, dX, dx_dt, K, 0, stream, go);
+        if (s == Q2D_OK) s = gemm_impl(qdY, 1, qX, 1, dW, dw_dt, K, accumulate_dw, stream, go);
+        if (s != Q2D_OK) return s;
+    }
+    return Q2D_OK;
 }
 
 q2d_status q2d_grouped_tensor_init(q2d_tensor *t, int64_t rows, int64_t cols, int32_t nseg, int32_t block,
@@ -359,6 +393,7 @@ q2d_status q2d_grouped_tensor_init(q2d_tensor *t, int64_t rows, int64_t cols, in
     const q2d_status s = check_dims(rows, cols);
     if (s != Q2D_OK) return s;
     if (block != 32) return Q2D_EUNSUPPORTED;
+    if (grouped_capacity(rows, nseg) > kMaxGroupedRows) return Q2D_EUNSUPPORTED;
     return q2d_tensor_init(t, Q2D_FMT_FP4_2D, grouped_capacity(rows, nseg), cols, block, bytes);
 }
 
@@ -375,6 +410,7 @@ q2d_status q2d_grouped_quantize(const void *x, q2d_dtype dt, int64_t rows, int64
     if (rmode != Q2D_RTN && rmode != Q2D_SR) return Q2D_EINVAL;
     if (block != 32) return Q2D_EUNSUPPORTED;
     const int64_t cap = grouped_capacity(rows, nseg);
+    if (cap > kMaxGroupedRows) return Q2D_EUNSUPPORTED;
     s = check_tensor(out, Q2D_FMT_FP4_2D, cap, cols);
     if (s != Q2D_OK) return s;
     if (out->block != 32) return Q2D_EUNSUPPORTED;
@@ -403,6 +439,7 @@ q2d_status q2d_grouped_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B
     if (s == Q2D_OK && total_rows > kMaxDim) s = Q2D_EUNSUPPORTED;
     if (s != Q2D_OK) return s;
     const int64_t cap = grouped_capacity(total_rows, nseg);
+    if (cap > kMaxGroupedRows) return Q2D_EUNSUPPORTED;
     const Layout la = layout_of(Q2D_FMT_FP4_2D, A->rows, A->cols), lb = layout_of(Q2D_FMT_FP4_2D, B->rows, B->cols);
     GemmArgs g = {};
     g.a1d = g.b1d = 0;

@@ -134,6 +134,31 @@ __device__ __forceinline__ void wave_prefix(int n, F f, int32_t *out)
     }
 }
 
+// Segment offsets as the kernels use them: out[i] = min(max(0, off[0], ..,
+// off[i]), total) for i = 0 .. n.  A valid table (ascending from 0 to total) is
+// unchanged; any other one becomes ascending and inside [0, total], so the
+// segments stay inside the input rows and their padded sizes inside the
+// grouped capacity.  Run by one full wave; n <= kMaxSegs.
+__device__ __forceinline__ void wave_offsets(int n, const int64_t *off, int64_t total, int32_t *out)
+{
+    const int lane = threadIdx.x & 63;
+    int32_t carry = 0;
+    for (int base = 0; base <= n; base += 64) {
+        const int i = base + lane;
+        int64_t o = i <= n ? off[i] : 0;
+        o = o < 0 ? 0 : (o > total ? total : o);
+        int32_t v = (int32_t)o;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int32_t u = __shfl_up(v, d);
+            if (lane >= d) v = max(v, u);
+        }
+        v = max(v, carry);
+        if (i <= n) out[i] = v;
+        carry = __shfl(v, 63);
+    }
+}
+
 // Largest e < n with table[e] <= x (table ascending, table[0] = 0 <= x).
 __device__ __forceinline__ int seg_search(const int32_t *table, int n, int32_t x)
 {

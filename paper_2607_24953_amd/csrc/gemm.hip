@@ -371,7 +371,7 @@ struct TileSpace {
     const GemmArgs &g;
     const GroupedArgs &gr;
     int32_t tiles_m, tiles_n;
-    const int32_t *pad_start, *tile_start;
+    const int32_t *pad_start, *tile_start, *seg_start;
     uint32_t total;        // tiles (ragged M: row tiles of all experts x column tiles)
     uint32_t per, rem, span;   // dense: XCD share of the tile order, group span
 
@@ -413,7 +413,8 @@ struct TileSpace {
             const int64_t p_e = __builtin_amdgcn_readfirstlane(pad_start[e]);
             t.a += p_e * g.lda;
             t.sa += (p_e / 32) * g.ldsa;
-            const int64_t o0 = gr.seg_offsets[e], o1 = gr.seg_offsets[e + 1];
+            const int64_t o0 = __builtin_amdgcn_readfirstlane(seg_start[e]);
+            const int64_t o1 = __builtin_amdgcn_readfirstlane(seg_start[e + 1]);
             t.M = (int32_t)(o1 - o0);
             t.c += o0 * g.ldc * esize;
             if (gr.b_group_rows) {
@@ -649,22 +650,25 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];
     __shared__ int32_t pad_start[GMODE == 0 ? 1 : kMaxSegs + 1];
     __shared__ int32_t tile_start[GMODE == 1 ? kMaxSegs + 1 : 1];
+    __shared__ int32_t seg_start[GMODE == 0 ? 1 : kMaxSegs + 1];     // sanitized segment offsets
     __shared__ __attribute__((aligned(16))) uint8_t qstrip[QOUT ? 4 * kQStrip : 16];
 
     uint32_t total = (uint32_t)(tiles_m * tiles_n);
     if (GMODE != 0) {
-        const int64_t *off = gr.seg_offsets;
         if ((threadIdx.x >> 6) == 0) {
-            wave_prefix(gr.nseg, [&](int i) { return (int32_t)((off[i + 1] - off[i] + 127) / 128 * 128); }, pad_start);
+            wave_offsets(gr.nseg, gr.seg_offsets, gr.total_rows, seg_start);
+            __builtin_amdgcn_wave_barrier();
+            const int32_t *off = seg_start;
+            wave_prefix(gr.nseg, [&](int i) { return (off[i + 1] - off[i] + 127) / 128 * 128; }, pad_start);
             if (GMODE == 1)
-                wave_prefix(gr.nseg, [&](int i) { return (int32_t)((off[i + 1] - off[i] + BM2 - 1) / BM2); }, tile_start);
+                wave_prefix(gr.nseg, [&](int i) { return (off[i + 1] - off[i] + BM2 - 1) / BM2; }, tile_start);
         }
         __syncthreads();
         if (GMODE == 1) total = (uint32_t)__builtin_amdgcn_readfirstlane(tile_start[gr.nseg]) * (uint32_t)tiles_n;
         else total = (uint32_t)(gr.nseg * tiles_m * tiles_n);
     }
     const uint32_t nb = (uint32_t)(tiles_m * tiles_n);
-    const TileSpace<GMODE, BF16OUT> ts{g, gr, tiles_m, tiles_n, pad_start, tile_start, total,
+    const TileSpace<GMODE, BF16OUT> ts{g, gr, tiles_m, tiles_n, pad_start, tile_start, seg_start, total,
                                        nb / kXcds, nb % kXcds, (uint32_t)(kGroupM * tiles_n)};
 
     const int tid = threadIdx.x, lane = tid & 63;

@@ -520,16 +520,19 @@ __attribute__((amdgpu_waves_per_eu(VEC && SR ? 3 : (VEC && !GROUPED ? 4 : 1)))) 
         // workgroup then walks the row tiles of all segments (tile = blockIdx.x,
         // + gridDim.x, ...) and narrows `a` to each tile's segment
         __shared__ int32_t pad_start[kMaxSegs + 1];
-        const int64_t *off = a.seg_offsets;
-        if ((threadIdx.x >> 6) == 0)
-            wave_prefix(a.nseg, [&](int i) { return (int32_t)((off[i + 1] - off[i] + 127) / 128 * 128); }, pad_start);
+        __shared__ int32_t off[kMaxSegs + 1];
+        if ((threadIdx.x >> 6) == 0) {
+            wave_offsets(a.nseg, a.seg_offsets, a.rows, off);
+            __builtin_amdgcn_wave_barrier();
+            wave_prefix(a.nseg, [&](int i) { return (off[i + 1] - off[i] + 127) / 128 * 128; }, pad_start);
+        }
         __syncthreads();
         const int64_t tiles = (int64_t)(pad_start[a.nseg] / kTile) * tiles_c;
         for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
             const int64_t rt = tile / tiles_c, tc = tile - rt * tiles_c;
             const int32_t prow = (int32_t)(rt * kTile);
             const int e = seg_search(pad_start, a.nseg, prow);
-            const int64_t r_begin = off[e], n_e = off[e + 1] - off[e];
+            const int64_t r_begin = off[e], n_e = (int64_t)off[e + 1] - off[e];
             const int32_t p_e = pad_start[e];
             QuantArgs b = a;
             b.x = reinterpret_cast<const uint8_t *>(a.x) + r_begin * a.stride_r * (int64_t)sizeof(T);

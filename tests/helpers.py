@@ -43,3 +43,11 @@ def as_oracle_tensor(q, rows, cols, fmt="fp4") -> dict:
     d = gpu_buffers(q)
     d["rows"], d["cols"] = rows, cols
     return d
+
+
+def grouped_written(q, P: int) -> dict:
+    """Host copy of the written region (the first P padded rows) of a grouped tensor."""
+    torch.cuda.synchronize()
+    return {"codes": q.codes[:P].cpu().numpy(), "scales": q.scales[:P // 32].cpu().numpy(),
+            "codes_t": q.codes_t[:, :P // 2].cpu().numpy(),
+            "scales_t": q.scales_t[:, :P // 32].cpu().numpy()}

@@ -155,6 +155,26 @@ int main()
            Q2D_OK, true);
     EXPECT(q2d_linear_fwd(x, x, Q2D_BF16, T, N, K + 1, Q2D_RTN, Q2D_RTN, 0, 0, 1, &qX, &qW, C, Q2D_F32, st),
            Q2D_EINVAL, false);
+    // a later step's bad argument stops the composite call before its first launch
+    EXPECT(q2d_linear_fwd(x, x, Q2D_BF16, T, N, K, Q2D_RTN, Q2D_RTN, 0, 0, 1, &qX, &qW, C, (q2d_dtype)7, st),
+           Q2D_EINVAL, false);                                                            // output dtype
+    EXPECT(q2d_linear_fwd(x, x, Q2D_BF16, T, N, K, Q2D_RTN, Q2D_RTN, 0, 0, 1, &qX, &qW, (char *)C + 2, Q2D_F32, st),
+           Q2D_EINVAL, false);                                                            // misaligned Y
+    EXPECT(q2d_linear_fwd(x, x, Q2D_BF16, T, N, K, Q2D_RTN, (q2d_round)9, 0, 0, 1, &qX, &qW, C, Q2D_F32, st),
+           Q2D_EINVAL, false);                                                            // W's rounding mode
+    q2d_tensor badW = qW;
+    badW.ld_codes -= 16;
+    EXPECT(q2d_linear_fwd(x, x, Q2D_BF16, T, N, K, Q2D_RTN, Q2D_RTN, 0, 0, 1, &qX, &badW, C, Q2D_F32, st),
+           Q2D_EINVAL, false);                                                            // W's layout
+    q2d_tensor q8X = tensor(Q2D_FMT_MXFP8, T, K, 32, 13);
+    EXPECT(q2d_linear_bwd(x, Q2D_BF16, &q8X, &qW, Q2D_SR, 0, 2, &qdY, C, Q2D_BF16, dev(62), Q2D_F32, 0, st),
+           Q2D_EINVAL, false);                                                            // MXFP8 X at the dW GEMM
+    EXPECT(q2d_linear_bwd(x, Q2D_BF16, &qX, &qW, Q2D_SR, 0, 2, &qdY, C, Q2D_BF16, dev(62), (q2d_dtype)9, 0, st),
+           Q2D_EINVAL, false);                                                            // dW dtype
+    EXPECT(q2d_linear_bwd(x, Q2D_BF16, &qX, &qW, Q2D_SR, 0, 2, &qdY, C, Q2D_BF16, dev(62), Q2D_F32, 2, st),
+           Q2D_EINVAL, false);                                                            // accumulate flag
+    EXPECT(q2d_linear_bwd(x, Q2D_BF16, &qX, &qW, Q2D_SR, 0, 2, &qdY, (char *)C + 1, Q2D_BF16, dev(62), Q2D_F32, 0,
+                          st), Q2D_EINVAL, false);                                        // misaligned dX
 
     // ---- grouped (MoE): 4 experts
     const int32_t E = 4;

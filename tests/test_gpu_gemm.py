@@ -265,10 +265,12 @@ def _sample_rows(qt_np, trans, rows, fmt="fp4"):
     raise ValueError(fmt)
 
 
-@pytest.mark.parametrize("name", ["dense_1b", "dense_7b"])
+@pytest.mark.parametrize("name", ["dense_1b", "dense_7b", "mixed_7b"])
 def test_full_launch_configuration(q2d, name):
-    """Every GEMM of the 1B-class (SR on all operands) and 7B-class (the benchmark's
-    15) linear workloads at full size (bf16 Y and dX, fp32 dW), 48 sampled rows each.
+    """Every FP4 GEMM of the 1B-class (SR on all operands), 7B-class (the benchmark's
+    15) and mixed 7B-class (V, O, gate, up and down in 2D-block FP4 with SR on X,
+    W and dY; its MXFP8 Q/K GEMMs have their own test) linear workloads at full
+    size (bf16 Y and dX, fp32 dW), 48 sampled rows each.
 
     The oracle quantizes the same inputs (byte-equal to the device operands);
     the device GEMMs are compared with float64 products of the oracle's
@@ -276,6 +278,8 @@ def test_full_launch_configuration(q2d, name):
     w = synth.WORKLOADS[name](device=DEV)
     rng = np.random.default_rng(0)
     for lin in w.linears:
+        if lin.fmt != "fp4":
+            continue
         X, W, dY = w.tensors[lin.x], w.tensors[lin.w], w.tensors[lin.dy]
         Y, qX, qW = q2d.q2d_linear_fwd(X, W, w.rounding[lin.x], w.rounding[lin.w], seed=w.seed,
                                        offset_x=0, offset_w=1, y_dtype=torch.bfloat16)

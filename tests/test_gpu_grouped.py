@@ -339,3 +339,59 @@ def test_full_moe_30b_launch_configuration(q2d):
     ragged_k("dY_d", "H", "down weight gradient")
     del ops, w
     torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------------ offsets the host cannot check
+
+# (device offsets, rows): descending entries, negative entries, entries beyond
+# the row count, a first entry above 0 and a last entry below the row count
+BAD_OFFSETS = [([-5, 100, 60, 300, 900, 650, 700], 700),
+               ([0, 50, 40, 200, 150], 260),
+               ([10, 500, 400, 420], 300)]
+
+
+def sanitized(off, rows):
+    """The table the kernels use: o'[i] = min(max(0, off[0..i]), rows)."""
+    return np.minimum(np.maximum.accumulate(np.maximum(np.asarray(off, np.int64), 0)), rows)
+
+
+@pytest.mark.parametrize("case", range(len(BAD_OFFSETS)))
+def test_invalid_offsets_stay_in_bounds(q2d, case):
+    """Offsets live on the device, so the C ABI cannot reject a bad table before
+    the launch.  The kernels use its sanitized form (ascending, inside
+    [0, rows]): the quantizer and both grouped GEMMs then give exactly the
+    results of that table, and nothing outside the buffers is touched."""
+    off, S = BAD_OFFSETS[case]
+    good = sanitized(off, S)
+    E = len(off) - 1
+    K, N = 256, 96
+    X = synth.normal((S, K), 1.0, 61 + case, torch.bfloat16, device=DEV)
+    dY = synth.normal((S, N), 1e-3, 62 + case, torch.bfloat16, device=DEV)
+    W = synth.normal((E * N, K), 0.02, 63, torch.bfloat16, device=DEV)
+    qX = q2d.q2d_grouped_quantize(X, dev_offsets(off), "rtn")
+    qdY = q2d.q2d_grouped_quantize(dY, dev_offsets(off), "rtn")
+    # the oracle's grouped form starts at row 0: hand it the rows the table covers
+    lo, hi = int(good[0]), int(good[-1])
+    oX = oracle.quantize_fp4_grouped(X.cpu()[lo:hi], good - lo, "rtn")
+    odY = oracle.quantize_fp4_grouped(dY.cpu()[lo:hi], good - lo, "rtn")
+    assert_grouped_equal(qX, oX, "X")
+    assert_grouped_equal(qdY, odY, "dY")
+    qW = q2d.q2d_quantize(W, "rtn")
+    Wf = oracle.operand(oracle.quantize_fp4_2d(W.cpu(), "rtn"), False)
+    Y = torch.full((S, N), 3.0, device=DEV)
+    q2d.q2d_grouped_gemm(qX, 0, qW, 0, dev_offsets(off), out=Y)
+    dW = torch.full((E * N, K), 3.0, device=DEV)
+    q2d.q2d_grouped_gemm(qdY, 1, qX, 1, dev_offsets(off), out=dW)
+    Y, dW = Y.cpu().numpy(), dW.cpu().numpy()
+    for e in range(E):
+        a, b = int(good[e]), int(good[e + 1])
+        rows = slice(e * N, (e + 1) * N)
+        if a == b:
+            assert np.all(dW[rows] == 0)
+            continue
+        ref = oracle.gemm(expert_rows(oX, good - lo, e), Wf[e * N:(e + 1) * N])
+        assert rel_frob(Y[a:b], ref) <= TOL, e
+        refw = oracle.gemm(expert_rows(odY, good - lo, e, True), expert_rows(oX, good - lo, e, True))
+        assert rel_frob(dW[rows], refw) <= TOL, e
+    # rows outside every segment are left as they were
+    assert np.all(Y[:lo] == 3.0) and np.all(Y[hi:] == 3.0)

@@ -76,6 +76,28 @@ def test_q2dlinear_matches_oracle(q2d, activations, block, dtype):
         assert rel_frob(lin.weight.grad.cpu().numpy(), ref["dW"]) <= 1e-5
 
 
+def test_default_layers_draw_independent_streams(q2d):
+    """Two layers built without a seed get different seeds, so the same output
+    gradient is rounded with different random bits in each (their dX differ);
+    two layers given one seed round it identically."""
+    from paper_2607_24953_amd.autograd import Q2DLinear
+    K, N = 128, 96
+    a, b = Q2DLinear(K, N, device=DEV), Q2DLinear(K, N, device=DEV)
+    c, d = Q2DLinear(K, N, seed=3, device=DEV), Q2DLinear(K, N, seed=3, device=DEV)
+    assert a.seed != b.seed
+    x = synth.normal((64, K), 1.0, 90, torch.float32, device=DEV)
+    dY = synth.normal((64, N), 1e-2, 91, torch.float32, device=DEV)
+    grads = []
+    for lin in (a, b, c, d):
+        with torch.no_grad():
+            lin.weight.copy_(a.weight)
+        xi = x.clone().requires_grad_()
+        lin(xi).backward(dY)
+        grads.append(xi.grad)
+    assert not torch.equal(grads[0], grads[1])
+    assert torch.equal(grads[2], grads[3])
+
+
 def _train(q2d, setting, steps=600, seed=0):
     from paper_2607_24953_amd.autograd import Q2DLinear
     T, K, N = 8192, 256, 256
