@@ -57,10 +57,11 @@ WORKLOAD_TEXT = {
                     "2D-block FP4 for X, W and dY (the larger block of the block-size trade-off; "
                     "X, W round-to-nearest; dY stochastic)",
     "dense_7b_yq_fused": "7B-class dense linears fwd+bwd (shapes and tensors of dense_7b) with every forward "
-                         "output Y delivered in 32x32 2D-block FP4 (round to nearest) for the next GEMM, "
-                         "quantized in the forward GEMM's epilogue",
-    "dense_7b_yq_separate": "the dense_7b_yq_fused step with Y written in bf16 by the forward GEMM and "
-                            "quantized by a separate quantizer launch",
+                         "output Y (round to nearest) and every data gradient dX (stochastic rounding) "
+                         "delivered in 32x32 2D-block FP4 for the next GEMM, quantized in the producing "
+                         "GEMM's epilogue",
+    "dense_7b_yq_separate": "the dense_7b_yq_fused step with Y and dX written in bf16 by their GEMMs and "
+                            "quantized by separate quantizer launches",
     "mixed_7b": "7B-class block fwd+bwd, tokens 16384: Q/K projections in MXFP8 (E4M3, 1x32) "
                 "and V, O, gate, up, down in 32x32 2D-block FP4 with stochastic rounding; "
                 "bf16 inputs with outlier channels",
@@ -69,6 +70,7 @@ WORKLOAD_TEXT = {
 # what each kind of launch is measured against
 KIND_PEAK = {"gemm_fp4": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
              "gemm_fp4_yq": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
+             "gemm_fp4_dxq": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
              "gemm_fp4_grouped": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
              # ragged-K weight gradients: per expert a short K and a float32 output
              # of E x N x K_in, so the output writes bound them
@@ -81,6 +83,7 @@ KIND_PEAK = {"gemm_fp4": ("mfma", PEAK_FP4_TFLOPS, "TFLOP/s"),
 KIND_KERNEL = {"gemm_fp4": "gemm_fp4_persistent_kernel", "gemm_fp4_grouped": "gemm_fp4_persistent_kernel (grouped)",
                "gemm_fp4_grouped_k": "gemm_fp4_persistent_kernel (grouped, ragged K)",
                "gemm_fp4_yq": "gemm_fp4_persistent_kernel (FP4-quantizing epilogue)",
+               "gemm_fp4_dxq": "gemm_fp4_persistent_kernel (FP4-quantizing epilogue, stochastic rounding)",
                "gemm_fp8": "gemm_fp8_256_kernel", "quant_fp4": "fp4_quantize_kernel",
                "quant_fp4_grouped": "fp4_quantize_kernel (grouped)",
                "quant_fp4_1d": "fp4_quantize_kernel (1D blocks)",
@@ -138,6 +141,7 @@ def gemm_bytes(a_elems, b_elems, c_bytes, fmt="fp4", a1d=False, b1d=False) -> fl
 
 
 KIND_SOURCES = {"gemm_fp4": "gemm.hip", "gemm_fp4_grouped": "gemm.hip", "gemm_fp4_grouped_k": "gemm.hip", "gemm_fp8": "gemm.hip", "gemm_fp4_yq": "gemm.hip",
+                "gemm_fp4_dxq": "gemm.hip",
                 "quant_fp4": "quantize_fp4.hip", "quant_fp4_grouped": "quantize_fp4.hip",
                 "quant_fp4_1d": "quantize_fp4.hip", "quant_mxfp8": "quantize_mxfp8.hip"}
 
@@ -151,8 +155,11 @@ def kind_of(kernel_name: str):
     import re
     m = re.search(r"gemm_fp4_persistent_kernel<([^>]*)>", kernel_name)
     if m:
-        # template arguments: bf16 output, accumulate, grouped mode, 1D operands, quantized output
+        # template arguments: bf16 output, accumulate, grouped mode, 1D operands, quantized
+        # output, stochastic rounding of it
         a = [t.strip() for t in m.group(1).split(",")]
+        if len(a) > 5 and a[5] == "true":
+            return "gemm_fp4_dxq"
         if len(a) > 4 and a[4] == "true":
             return "gemm_fp4_yq"
         return {"0": "gemm_fp4", "1": "gemm_fp4_grouped"}.get(a[2], "gemm_fp4_grouped_k")
@@ -266,6 +273,15 @@ class Step:
                     self.ops.append(("gemm_fp4_yq", "%s.%s" % (lin.name, nm), f, ab,
                                      lambda a=a, b=b, qy=qy: q2d.q2d_gemm_quantized(a, 0, b, 0, "rtn", out=qy)))
                     continue
+                if nm == "dX" and y_out == "fused":
+                    # dX leaves stochastically rounded, keyed by its own storage index
+                    qdx = q2d.QTensor(q2d.FP4_2D, T, K, dev)
+                    ab = gemm_bytes(M_ * K_, N_ * K_, M_ * N_ * (1.0 + 2.0 / 1024.0), lin.fmt, a1, b1)
+                    off = 100 + len(self.ops)
+                    self.ops.append(("gemm_fp4_dxq", "%s.%s" % (lin.name, nm), f, ab,
+                                     lambda a=a, b=b, q=qdx, off=off:
+                                     q2d.q2d_gemm_quantized(a, 0, b, 1, "sr", out=q, seed=w.seed, offset=off)))
+                    continue
                 ab = gemm_bytes(M_ * K_, N_ * K_, out.numel() * out.element_size(), lin.fmt, a1, b1)
                 self.ops.append((kind, "%s.%s" % (lin.name, nm), f, ab,
                                  lambda a=a, ta=ta, b=b, tb=tb, out=out:
@@ -275,6 +291,12 @@ class Step:
                     qb = quant_bytes(Y)
                     self.ops.append(("quant_fp4", "%s.Y" % lin.name, qb, qb,
                                      lambda Y=Y, qy=qy: q2d.q2d_quantize(Y, "rtn", out=qy)))
+                if nm == "dX" and y_out == "separate":
+                    qdx = q2d.QTensor(q2d.FP4_2D, T, K, dev)
+                    qb = quant_bytes(dX)
+                    off = 100 + len(self.ops)
+                    self.ops.append(("quant_fp4", "%s.dX" % lin.name, qb, qb,
+                                     lambda dX=dX, q=qdx, off=off: q2d.q2d_quantize(dX, "sr", w.seed, off, out=q)))
         self.flops = float(w.gemm_flops)
 
     def _moe(self):
@@ -414,7 +436,8 @@ PROFILE_FILES = {
     "dense_7b_1d": [("fp4_1d_kernels.dense_7b_1d.md", ("quant_fp4_1d", "gemm_fp4", "quant_fp4"))],
     "mixed_7b": [("mxfp8_kernels.mixed_7b.md", ("gemm_fp8", "quant_mxfp8", "gemm_fp4", "quant_fp4"))],
     "dense_7b_b64": [("block64_kernels.dense_7b_b64.md", ("quant_fp4", "gemm_fp4"))],
-    "dense_7b_yq_fused": [("gemm_fp4_yq.dense_7b_yq_fused.md", ("gemm_fp4_yq", "gemm_fp4", "quant_fp4"))],
+    "dense_7b_yq_fused": [("gemm_fp4_yq.dense_7b_yq_fused.md", ("gemm_fp4_yq", "gemm_fp4_dxq", "gemm_fp4",
+                                                                 "quant_fp4"))],
     "dense_7b_yq_separate": [("gemm_fp4_yq.dense_7b_yq_separate.md", ("gemm_fp4", "quant_fp4"))],
 }
 PROFILE_COMMANDS = """cd /tmp && export TMPDIR=/tmp; R=/root/repo; O=${PROFILE_OUT:-$R/profile_runs}; mkdir -p $O

@@ -239,17 +239,23 @@ q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int tr
  * tile's registers.
  *
  * A, B, transA, transB as for q2d_gemm (FP4_2D and FP4_1D operands).
- * mode     Q2D_RTN (Q2D_SR: Q2D_EUNSUPPORTED; stochastic rounding of a GEMM
- *          output is left to q2d_quantize).
+ * mode     Q2D_RTN, or Q2D_SR for an output that is a gradient (App. E: the
+ *          data gradient dX is the next layer's output gradient, which the
+ *          method rounds stochastically).  SR follows q2d_quantize's contract
+ *          for a row-major M x N tensor: element (r, c) has storage index
+ *          r N + c and draws its 16 bits from the Philox stream (seed,
+ *          offset), so the codes equal q2d_quantize(C, SR, seed, offset) of the
+ *          float32 result.  N must be a multiple of 8 for SR.
+ * seed, offset  the SR stream (ignored for Q2D_RTN).
  * out      descriptor from q2d_tensor_init(FP4_2D, M, N, 32) with all four
  *          buffers attached; written as q2d_quantize writes it (padding
  *          included).  A block holding a NaN or an infinity gets scale 0xFF
  *          and zero codes.
- * Q2D_EUNSUPPORTED for MXFP8 operands, block 64 output, or operands beyond
- * 4 GiB.  Stream-ordered.
+ * Q2D_EUNSUPPORTED for MXFP8 operands, block 64 output, SR with N not a
+ * multiple of 8, or operands beyond 4 GiB.  Stream-ordered.
  */
 q2d_status q2d_gemm_quantized(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, q2d_round mode,
-                              q2d_tensor *out, hipStream_t stream);
+                              uint64_t seed, uint64_t offset, q2d_tensor *out, hipStream_t stream);
 
 /*
  * Forward pass of a quantized linear layer Y = X W^T (Sec. 3; App. C):

@@ -456,15 +456,16 @@ def gemm(a: np.ndarray, b: np.ndarray) -> np.ndarray:
     return np.asarray(a, dtype=np.float64) @ np.asarray(b, dtype=np.float64).T
 
 
-def gemm_quantized(a: np.ndarray, b: np.ndarray) -> dict:
+def gemm_quantized(a: np.ndarray, b: np.ndarray, mode: str = "rtn", seed: int = 0, offset: int = 0) -> dict:
     """A GEMM whose result is quantized (App. C: a layer's output is the next
     GEMM's operand): C = A B^T in float64, rounded once to float32 (the
-    precision the result has before it is quantized), then 2D-block FP4 with
-    round to nearest."""
+    precision the result has before it is quantized), then 2D-block FP4 of the
+    row-major M x N result: round to nearest, or stochastic rounding with the
+    stream (seed, offset) for a gradient output (App. E)."""
     c = gemm(a, b)
     with np.errstate(over="ignore"):
         c32 = c.astype(np.float32)
-    return quantize_fp4_2d(np.ascontiguousarray(c32), "rtn")
+    return quantize_fp4_2d(np.ascontiguousarray(c32), mode, seed, offset)
 
 
 def linear(qx: dict, qw: dict, qdy: dict, fmt: str = "fp4", fmt_x: str | None = None) -> dict:

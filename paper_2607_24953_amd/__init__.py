@@ -62,7 +62,7 @@ def _load():
     L.q2d_grouped_quantize.argtypes = [P, I32, I64, I64, I64, I32, P, I32, I32, U64, U64, TP, P]
     L.q2d_grouped_gemm.argtypes = [TP, I32, TP, I32, I32, P, I64, P, I32, I64, I32, P]
     L.q2d_dequantize.argtypes = [TP, I32, P, I32, I64, P, I64, P]
-    L.q2d_gemm_quantized.argtypes = [TP, I32, TP, I32, I32, TP, P]
+    L.q2d_gemm_quantized.argtypes = [TP, I32, TP, I32, I32, U64, U64, TP, P]
     L.q2d_status_string.argtypes = [I32]
     L.q2d_status_string.restype = ctypes.c_char_p
     for name in ("q2d_tensor_init", "q2d_quantize", "mxfp8_quantize", "q2d_gemm",
@@ -240,16 +240,18 @@ def q2d_gemm(A: QTensor, transA: int, B: QTensor, transB: int, out: torch.Tensor
 
 
 def q2d_gemm_quantized(A: QTensor, transA: int, B: QTensor, transB: int, mode="rtn",
-                       out: QTensor | None = None) -> QTensor:
-    """op(A) op(B)^T quantized to 2D-block FP4 (round to nearest) in the GEMM's
-    epilogue; returns the quantized result with both orientations."""
+                       out: QTensor | None = None, seed: int = 0, offset: int = 0) -> QTensor:
+    """op(A) op(B)^T quantized to 2D-block FP4 in the GEMM's epilogue (round to
+    nearest, or stochastic rounding with the stream (seed, offset) keyed by the
+    row-major storage index of the M x N result); returns the quantized result
+    with both orientations."""
     M = A.cols if transA else A.rows
     N = B.cols if transB else B.rows
     if out is None:
         out = QTensor(FP4_2D, M, N, A.device)
     _same_device(A.device, B, out)
-    _check(_lib.q2d_gemm_quantized(A.ptr(), int(transA), B.ptr(), int(transB), _ROUND[mode], out.ptr(),
-                                   _stream(A.device)), "q2d_gemm_quantized")
+    _check(_lib.q2d_gemm_quantized(A.ptr(), int(transA), B.ptr(), int(transB), _ROUND[mode], int(seed),
+                                   int(offset), out.ptr(), _stream(A.device)), "q2d_gemm_quantized")
     return out
 
 

@@ -327,10 +327,10 @@ q2d_status q2d_gemm(const q2d_tensor *A, int transA, const q2d_tensor *B, int tr
 }
 
 q2d_status q2d_gemm_quantized(const q2d_tensor *A, int transA, const q2d_tensor *B, int transB, q2d_round mode,
-                              q2d_tensor *out, hipStream_t stream)
+                              uint64_t seed, uint64_t offset, q2d_tensor *out, hipStream_t stream)
 {
     if (!A || !B || !out) return Q2D_EINVAL;
-    if (mode != Q2D_RTN) return mode == Q2D_SR ? Q2D_EUNSUPPORTED : Q2D_EINVAL;
+    if (mode != Q2D_RTN && mode != Q2D_SR) return Q2D_EINVAL;
     GemmArgs g;
     bool fp4 = false;
     q2d_status s = gemm_operands(A, transA, B, transB, g, fp4);
@@ -340,6 +340,11 @@ q2d_status q2d_gemm_quantized(const q2d_tensor *A, int transA, const q2d_tensor 
     if (s != Q2D_OK) return s;
     if (out->block != 32) return Q2D_EUNSUPPORTED;
     if (!out->codes || !out->codes_t) return Q2D_EINVAL;
+    // stochastic rounding: the Philox blocks of 8 storage indices stay inside one row
+    if (mode == Q2D_SR && (g.N % 8) != 0) return Q2D_EUNSUPPORTED;
+    g.qsr = mode == Q2D_SR;
+    g.seed = seed;
+    g.offset = offset;
     // the epilogue stores 8-byte runs of codes_t
     if (!aligned(out->codes_t, 16) || (out->ld_codes_t % 16) != 0) return Q2D_EINVAL;
     g.qc = out->codes; g.ldqc = out->ld_codes;

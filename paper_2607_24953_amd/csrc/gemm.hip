@@ -22,6 +22,7 @@
 // row tiles for operand reuse.
 #include <atomic>
 #include <type_traits>
+#include <utility>
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -504,12 +505,59 @@ __device__ __forceinline__ void store_block(v16f (&acc)[4][4], uint8_t *cbase, u
 //      then the strip leaves as 16-byte row segments.
 // Only the written extent of the layout is touched: codes rows < M, bytes below
 // roundup(N, 128) / 2; codes_t rows < N, bytes below roundup(M, 128) / 2.
+//
+// Stochastic rounding (SR): element (r, c) of the M x N result takes the draw of
+// storage index r N + c of a row-major M x N tensor (half (idx & 1) of word
+// (idx & 7) >> 1 of the Philox block for counter (idx >> 3, offset)), the draw
+// q2d_quantize would give it, and is converted on its own with seed r16 << 16
+// (first element of a pair) or r16 << 15 (second).  N is a multiple of 8, so a
+// Philox block covers 8 consecutive columns of one row: the wave computes each
+// of a tile's 128 blocks once (two per lane) into its LDS table, and every lane
+// reads back the 16-bit draws of the 16 elements it holds.
+// f(std::integral_constant<int, 0>) ... f(std::integral_constant<int, N - 1>), in order
+template <typename F, int... Is>
+__device__ __forceinline__ void unroll_seq(F &&f, std::integer_sequence<int, Is...>)
+{
+    (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void unroll(F &&f)
+{
+    unroll_seq(f, std::make_integer_sequence<int, N>{});
+}
+
 constexpr int kQPitch = 80;                     // LDS strip row pitch (64 bytes + pad)
 constexpr int kQStrip = 32 * kQPitch;           // per wave
+constexpr int kPRow = 80;                       // Philox table row: four 16-byte blocks + pad
+constexpr int kPTab = 32 * kPRow;               // per wave
 
-template <bool CHECK>
-__device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &g, uint8_t *strip, int r0, int c0,
-                                             int rows_left, int cols_left)
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// SR conversion of a pair into byte `sel` of a zero word (only the nibble the
+// caller keeps is defined)
+__device__ __forceinline__ uint32_t sr_cvt(int sel, f32x2 v, uint32_t seed, float scale)
+{
+    switch (sel) {
+    case 0: return __builtin_amdgcn_cvt_scalef32_sr_pk_fp4_f32(0u, v, seed, scale, 0);
+    case 1: return __builtin_amdgcn_cvt_scalef32_sr_pk_fp4_f32(0u, v, seed, scale, 1);
+    case 2: return __builtin_amdgcn_cvt_scalef32_sr_pk_fp4_f32(0u, v, seed, scale, 2);
+    default: return __builtin_amdgcn_cvt_scalef32_sr_pk_fp4_f32(0u, v, seed, scale, 3);
+    }
+}
+
+// byte `sel` of `old` gets the SR codes of the pair (a, b): a with seed ra
+// (= r16 << 16) in the low nibble, b with seed rb >> 1 (= r16 << 15) in the high
+__device__ __forceinline__ uint32_t sr_pair_into(uint32_t old, int sel, float a, float b, uint32_t ra, uint32_t rb,
+                                                 float scale)
+{
+    const f32x2 v = {a, b};
+    const uint32_t lo = sr_cvt(sel, v, ra, scale), hi = sr_cvt(sel, v, rb >> 1, scale);
+    return old | (lo & (0x0Fu << (8 * sel))) | (hi & (0xF0u << (8 * sel)));
+}
+
+template <bool CHECK, bool SR>
+__device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &g, uint8_t *strip, uint8_t *ptab,
+                                             int r0, int c0, int rows_left, int cols_left)
 {
     const int lane = threadIdx.x & 63;
     const int col = lane & 31, h = lane >> 5, odd = lane & 1;
@@ -555,11 +603,12 @@ __device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &
 #pragma unroll
             for (int j = 0; j < 4; ++j) am[i][j] = max(am[i][j], (uint32_t)__shfl_xor((int)am[i][j], m));
 
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    // compile-time tile indices: a runtime loop here would put acc in scratch memory
+    unroll<4>([&](auto ic) __attribute__((always_inline)) {
+        constexpr int i = decltype(ic)::value;
         const int tr = r0 + 32 * i;                     // strip origin row in C
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        unroll<4>([&](auto jc) __attribute__((always_inline)) {
+            constexpr int j = decltype(jc)::value;
             const int tc = c0 + 32 * j;                 // tile origin column
             const bool finite = am[i][j] < 0x7F800000u;
             const int e = fp4_block_exponent(am[i][j]);
@@ -567,16 +616,48 @@ __device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &
             float v[16];
 #pragma unroll
             for (int r = 0; r < 16; ++r) v[r] = value(i, j, r);
+            // SR draws (<< 16) of the lane's elements (rows 8 (r / 4) + 4 h + r % 4, column
+            // col), read from the wave's table where a conversion needs them
+            const int cofs = 16 * (col >> 3) + 4 * ((col & 7) >> 1) + 2 * (col & 1);
+            auto rr = [&](int r) __attribute__((always_inline)) -> uint32_t {
+                const int rl = 8 * (r >> 2) + 4 * h + (r & 3);
+                return (uint32_t)*reinterpret_cast<const uint16_t *>(ptab + rl * kPRow + cofs) << 16;
+            };
+            if constexpr (SR) {
+                // the previous tile's reads of the table come first (in program order)
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+                    const int b = lane + 64 * t, brow = b >> 2, bcg = b & 3;
+                    const uint64_t idx = (uint64_t)(uint32_t)(tr + brow) * (uint64_t)g.N + (uint64_t)(tc + 8 * bcg);
+                    uint32_t w[4];
+                    philox4x32_10((uint32_t)(idx >> 3), (uint32_t)(idx >> 35), (uint32_t)g.offset,
+                                  (uint32_t)(g.offset >> 32), (uint32_t)g.seed, (uint32_t)(g.seed >> 32), w);
+                    *reinterpret_cast<uint4 *>(ptab + brow * kPRow + 16 * bcg) = make_uint4(w[0], w[1], w[2], w[3]);
+                }
+                // LDS accesses of one wave complete in order: the reads below see the table
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_sched_barrier(0);
+            }
             // column-packed: word q/2 byte 2 (q % 2) + k holds rows (8q + 4h + 2k, +1)
             uint32_t w0 = 0, w1 = 0;
-            w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[0], v[1], scale, 0);
-            w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[2], v[3], scale, 1);
-            w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[4], v[5], scale, 2);
-            w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[6], v[7], scale, 3);
-            w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[8], v[9], scale, 0);
-            w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[10], v[11], scale, 1);
-            w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[12], v[13], scale, 2);
-            w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[14], v[15], scale, 3);
+            if constexpr (SR) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    w0 = sr_pair_into(w0, k, v[2 * k], v[2 * k + 1], rr(2 * k), rr(2 * k + 1), scale);
+                    w1 = sr_pair_into(w1, k, v[8 + 2 * k], v[9 + 2 * k], rr(8 + 2 * k), rr(9 + 2 * k), scale);
+                }
+            } else {
+                w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[0], v[1], scale, 0);
+                w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[2], v[3], scale, 1);
+                w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[4], v[5], scale, 2);
+                w0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w0, v[6], v[7], scale, 3);
+                w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[8], v[9], scale, 0);
+                w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[10], v[11], scale, 1);
+                w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[12], v[13], scale, 2);
+                w1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w1, v[14], v[15], scale, 3);
+            }
             if (!finite) w0 = w1 = 0;
             // half 0 stores bytes 0..7 of the run (q = 0, 1 of both halves), half 1
             // bytes 8..15 (q = 2, 3)
@@ -596,11 +677,21 @@ __device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &
                 const float own = odd ? v[8 + k] : v[k];
                 const float lo = odd ? nb : own, hi = odd ? own : nb;
                 uint32_t &w = rowb[k >> 2];
-                switch (k & 3) {
-                case 0: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 0); break;
-                case 1: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 1); break;
-                case 2: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 2); break;
-                default: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 3); break;
+                if constexpr (SR) {
+                    // the neighbour's draw travels with its value
+                    const uint32_t r_lo = rr(k), r_hi = rr(8 + k);
+                    const uint32_t sendr = odd ? r_lo : r_hi;
+                    const uint32_t nbr = (uint32_t)__builtin_amdgcn_update_dpp((int)sendr, (int)sendr, 0xB1, 0xF, 0xF,
+                                                                               false);
+                    const uint32_t ownr = odd ? r_hi : r_lo;
+                    w = sr_pair_into(w, k & 3, lo, hi, odd ? nbr : ownr, odd ? ownr : nbr, scale);
+                } else {
+                    switch (k & 3) {
+                    case 0: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 0); break;
+                    case 1: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 1); break;
+                    case 2: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 2); break;
+                    default: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 3); break;
+                    }
                 }
             }
             if (!finite) rowb[0] = rowb[1] = 0;
@@ -615,7 +706,7 @@ __device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &
                 if (tr < g.M && tc < padn) g.qs[(int64_t)(tr / 32) * g.ldqs + tc / 32] = sbyte;
                 if (tc < g.N && tr < padm) g.qst[(int64_t)(tc / 32) * g.ldqst + tr / 32] = sbyte;
             }
-        }
+        });
         // the strip's 32 rows x 64 bytes as 16-byte row segments (LDS accesses of
         // one wave complete in order, so the reads see the writes above)
         __builtin_amdgcn_wave_barrier();
@@ -628,7 +719,7 @@ __device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &
         }
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_sched_barrier(0);
-    }
+    });
 }
 
 // SM: bit 0 -- A has 1x32 blocks (one scale per row and K-group: activations
@@ -636,7 +727,7 @@ __device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &
 // GEMM).  Such an operand's per-row scale words follow the 2D words in each
 // stage (1 KB per operand, one load per wave) and every lane reads its own
 // row's word instead of the block row's.
-template <bool BF16OUT, bool ACC, int GMODE, int SM, bool QOUT = false>
+template <bool BF16OUT, bool ACC, int GMODE, int SM, bool QOUT = false, bool QSR = false>
 __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmArgs g, int tiles_m, int tiles_n,
                                                                           const GroupedArgs gr)
 {
@@ -652,6 +743,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     __shared__ int32_t tile_start[GMODE == 1 ? kMaxSegs + 1 : 1];
     __shared__ int32_t seg_start[GMODE == 0 ? 1 : kMaxSegs + 1];     // sanitized segment offsets
     __shared__ __attribute__((aligned(16))) uint8_t qstrip[QOUT ? 4 * kQStrip : 16];
+    __shared__ __attribute__((aligned(16))) uint8_t ptab[QSR ? 4 * kPTab : 16];
 
     uint32_t total = (uint32_t)(tiles_m * tiles_n);
     if (GMODE != 0) {
@@ -690,10 +782,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
         const int r0 = t.m0 + wm * 128, c0 = t.n0 + wn * 128;
         if constexpr (QOUT) {
             uint8_t *strip = qstrip + wave * kQStrip;
+            uint8_t *tab = ptab + (QSR ? wave * kPTab : 0);
             if (t.m0 + BM2 <= t.M && t.n0 + BN2 <= t.N)
-                store_qblock<false>(acc, g, strip, r0, c0, 128, 128);
+                store_qblock<false, QSR>(acc, g, strip, tab, r0, c0, 128, 128);
             else
-                store_qblock<true>(acc, g, strip, r0, c0, t.M - r0, t.N - c0);
+                store_qblock<true, QSR>(acc, g, strip, tab, r0, c0, t.M - r0, t.N - c0);
         } else {
             uint8_t *cb = t.c + (int64_t)r0 * ldc_bytes + (int64_t)c0 * esize;
             if (t.m0 + BM2 <= t.M && t.n0 + BN2 <= t.N)
@@ -1121,34 +1214,40 @@ hipError_t launch_gemm(const GemmArgs &g, int fmt, int c_is_bf16, hipStream_t st
     return c_is_bf16 ? launch_t<kFmtMxfp8, true>(g, stream) : launch_t<kFmtMxfp8, false>(g, stream);
 }
 
+namespace {
+
+template <int SM, bool QSR>
+void launch_quantized_t(const GemmArgs &g, int tm, int tn, int64_t grid, hipStream_t stream)
+{
+    const GroupedArgs none = {nullptr, 0, 0, 0, 0, 0};
+    hipLaunchKernelGGL((gemm_fp4_persistent_kernel<false, false, 0, SM, true, QSR>), dim3((unsigned)grid),
+                       dim3(kThreads), 0, stream, g, tm, tn, none);
+}
+
+template <bool QSR>
+void launch_quantized_sm(const GemmArgs &g, int tm, int tn, int64_t grid, hipStream_t stream)
+{
+    switch ((g.a1d ? 1 : 0) | (g.b1d ? 2 : 0)) {
+    case 0: launch_quantized_t<0, QSR>(g, tm, tn, grid, stream); break;
+    case 1: launch_quantized_t<1, QSR>(g, tm, tn, grid, stream); break;
+    case 2: launch_quantized_t<2, QSR>(g, tm, tn, grid, stream); break;
+    default: launch_quantized_t<3, QSR>(g, tm, tn, grid, stream); break;
+    }
+}
+
+}  // namespace
+
 hipError_t launch_gemm_quantized(const GemmArgs &g, hipStream_t stream)
 {
     const bool off32 = g.M * g.lda <= (int64_t(1) << 32) && g.N * g.ldb <= (int64_t(1) << 32);
     if (!off32) return hipErrorInvalidValue;
-    const GroupedArgs none = {nullptr, 0, 0, 0, 0, 0};
     const int tm = (int)((g.M + BM2 - 1) / BM2), tn = (int)((g.N + BN2 - 1) / BN2);
     int64_t grid = cu_count();
     const int64_t tiles = (int64_t)tm * tn;
     grid = grid < tiles ? grid : tiles;
     grid = (grid + kXcds - 1) / kXcds * kXcds;
-    switch ((g.a1d ? 1 : 0) | (g.b1d ? 2 : 0)) {
-    case 0:
-        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<false, false, 0, 0, true>), dim3((unsigned)grid), dim3(kThreads),
-                           0, stream, g, tm, tn, none);
-        break;
-    case 1:
-        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<false, false, 0, 1, true>), dim3((unsigned)grid), dim3(kThreads),
-                           0, stream, g, tm, tn, none);
-        break;
-    case 2:
-        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<false, false, 0, 2, true>), dim3((unsigned)grid), dim3(kThreads),
-                           0, stream, g, tm, tn, none);
-        break;
-    default:
-        hipLaunchKernelGGL((gemm_fp4_persistent_kernel<false, false, 0, 3, true>), dim3((unsigned)grid), dim3(kThreads),
-                           0, stream, g, tm, tn, none);
-        break;
-    }
+    if (g.qsr) launch_quantized_sm<true>(g, tm, tn, grid, stream);
+    else launch_quantized_sm<false>(g, tm, tn, grid, stream);
     return hipGetLastError();
 }
 

@@ -56,6 +56,10 @@ struct GemmArgs {
     uint8_t *qct; int64_t ldqct;        // codes_t [N][ldqct]
     uint8_t *qs;  int64_t ldqs;         // scales [ceil(M/32)][ldqs]
     uint8_t *qst; int64_t ldqst;        // scales_t [ceil(N/32)][ldqst]
+    // stochastic rounding of the quantized output: element (r, c) draws the
+    // 16-bit value of storage index r * N + c from the Philox stream (seed, offset)
+    int qsr;
+    uint64_t seed, offset;
 };
 
 enum GemmFmt { kFmtFp4Block2D = 0, kFmtMxfp8 = 1 };

@@ -28,7 +28,7 @@ import torch
 
 __all__ = [
     "normal", "add_outlier_channels", "moe_counts", "segment_offsets",
-    "Workload", "student_t", "regression_task", "tiny", "dense_1b", "dense_7b", "dense_7b_1d", "dense_7b_b64", "dense_7b_yq", "moe_30b", "mixed_7b", "WORKLOADS",
+    "Workload", "student_t", "regression_task", "sparse_regression_task", "tiny", "dense_1b", "dense_7b", "dense_7b_1d", "dense_7b_b64", "dense_7b_yq", "moe_30b", "mixed_7b", "WORKLOADS",
 ]
 
 
@@ -88,6 +88,22 @@ def regression_task(tokens: int, k_in: int, n_out: int, noise: float, nu: int, s
     if noise:
         Y = Y + noise * student_t((tokens, n_out), nu, seed + 2, device)
     return X, W, Y
+
+
+def sparse_regression_task(tokens: int, k_in: int, n_out: int, nnz: int, lo: float, hi: float,
+                           background: float, seed: int, device="cpu"):
+    """Teacher-student linear regression on sparse large features: every row of
+    X has `nnz` entries of magnitude uniform in [lo, hi) with random signs at
+    random positions, the rest N(0, background^2); teacher W* ~ N(0, 1/k_in);
+    targets X W*^T (no noise).  Returns float32 (X, W*, Y)."""
+    g = _gen(seed, device)
+    X = background * torch.randn((tokens, k_in), generator=g, device=device, dtype=torch.float32)
+    pos = torch.rand((tokens, k_in), generator=g, device=device).argsort(dim=1)[:, :nnz]
+    mag = lo + (hi - lo) * torch.rand((tokens, nnz), generator=g, device=device)
+    sgn = torch.where(torch.rand((tokens, nnz), generator=g, device=device) < 0.5, -1.0, 1.0)
+    X.scatter_(1, pos, mag * sgn)
+    W = normal((n_out, k_in), 1.0 / float(k_in) ** 0.5, seed + 1, torch.float32, device)
+    return X, W, X @ W.t()
 
 
 def moe_counts(tokens: int = 16384, experts: int = 128, topk: int = 8,
@@ -228,9 +244,10 @@ def dense_7b_b64(device="cpu") -> Workload:
 
 
 def dense_7b_yq(device="cpu", fused: bool = True) -> Workload:
-    """The dense_7b tensors and linears with every forward output Y delivered in
-    2D-block FP4 (round to nearest) for the next GEMM: quantized in the forward
-    GEMM's epilogue (fused) or by a separate quantization of the bf16 Y."""
+    """The dense_7b tensors and linears with every forward output Y (round to
+    nearest) and every data gradient dX (stochastic rounding) delivered in
+    2D-block FP4 for the next GEMM: quantized in the producing GEMM's epilogue
+    (fused) or by a separate quantization of the bf16 result."""
     w = dense_7b(device)
     w.extra["y_out"] = "fused" if fused else "separate"
     w.name = "dense_7b_yq_fused" if fused else "dense_7b_yq_separate"

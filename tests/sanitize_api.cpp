@@ -141,10 +141,16 @@ int main()
     Wrow.scales_t = nullptr;
     EXPECT(q2d_gemm(&dY, 0, &Wrow, 1, C, Q2D_BF16, K, 0, st), Q2D_EINVAL, false);     // no column copy
     q2d_tensor Y = tensor(Q2D_FMT_FP4_2D, T, N, 32, 8);
-    EXPECT(q2d_gemm_quantized(&X, 0, &W, 0, Q2D_RTN, &Y, st), Q2D_OK, true);
-    EXPECT(q2d_gemm_quantized(&X, 0, &W, 0, Q2D_SR, &Y, st), Q2D_EUNSUPPORTED, false);
-    EXPECT(q2d_gemm_quantized(&X, 0, &W, 0, Q2D_RTN, &dY, st), Q2D_OK, true);           // same shape
-    EXPECT(q2d_gemm_quantized(&X, 0, &W, 0, Q2D_RTN, &X, st), Q2D_EINVAL, false);
+    EXPECT(q2d_gemm_quantized(&X, 0, &W, 0, Q2D_RTN, 0, 0, &Y, st), Q2D_OK, true);
+    EXPECT(q2d_gemm_quantized(&X, 0, &W, 0, Q2D_SR, 5, 7, &Y, st), Q2D_EUNSUPPORTED, false);   // N % 8 != 0
+    q2d_tensor W8 = tensor(Q2D_FMT_FP4_2D, 704, K, 32, 14), Y8 = tensor(Q2D_FMT_FP4_2D, T, 704, 32, 16);
+    EXPECT(q2d_gemm_quantized(&X, 0, &W8, 0, Q2D_SR, 5, 7, &Y8, st), Q2D_OK, true);
+    CHECK(q2d::g_gemm.qsr == 1 && q2d::g_gemm.seed == 5 && q2d::g_gemm.offset == 7, "quantized SR stream");
+    EXPECT(q2d_gemm_quantized(&X, 0, &W, 0, Q2D_RTN, 5, 7, &Y, st), Q2D_OK, true);
+    CHECK(q2d::g_gemm.qsr == 0, "quantized RTN");
+    EXPECT(q2d_gemm_quantized(&X, 0, &W, 0, (q2d_round)3, 0, 0, &Y, st), Q2D_EINVAL, false);
+    EXPECT(q2d_gemm_quantized(&X, 0, &W, 0, Q2D_RTN, 0, 0, &dY, st), Q2D_OK, true);     // same shape
+    EXPECT(q2d_gemm_quantized(&X, 0, &W, 0, Q2D_RTN, 0, 0, &X, st), Q2D_EINVAL, false);
 
     // ---- linear layer
     q2d_tensor qX = tensor(Q2D_FMT_FP4_2D, T, K, 32, 9), qW = tensor(Q2D_FMT_FP4_2D, N, K, 32, 10);

@@ -156,18 +156,20 @@ def test_gemm_quantized_error_paths(q2d):
         return d
     a, b, out = t(0, 64, 96), t(0, 128, 96), t(0, 64, 128)
     P = ctypes.byref
-    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 1, P(out), None) == 2          # SR
-    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 5, P(out), None) == 1          # bad mode
-    assert L.q2d_gemm_quantized(None, 0, P(b), 0, 0, P(out), None) == 1
-    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 0, None, None) == 1
-    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 0, P(t(0, 64, 127)), None) == 1   # shape
-    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 0, P(t(0, 64, 128, 64)), None) == 2  # block 64 output
-    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 0, P(t(2, 64, 128)), None) == 1   # 1D output
-    assert L.q2d_gemm_quantized(P(t(1, 64, 96)), 0, P(t(1, 128, 96)), 0, 0, P(out), None) == 2   # MXFP8
+    Q = lambda A, ta, B, tb, mode, o: L.q2d_gemm_quantized(A, ta, B, tb, mode, 0, 0, o, None)
+    b130 = t(0, 130, 96)
+    assert Q(P(a), 0, P(b130), 0, 1, P(t(0, 64, 130))) == 2                # SR needs N % 8 == 0
+    assert Q(P(a), 0, P(b), 0, 5, P(out)) == 1                             # bad mode
+    assert Q(None, 0, P(b), 0, 0, P(out)) == 1
+    assert Q(P(a), 0, P(b), 0, 0, None) == 1
+    assert Q(P(a), 0, P(b), 0, 0, P(t(0, 64, 127))) == 1                   # shape
+    assert Q(P(a), 0, P(b), 0, 0, P(t(0, 64, 128, 64))) == 2               # block 64 output
+    assert Q(P(a), 0, P(b), 0, 0, P(t(2, 64, 128))) == 1                   # 1D output
+    assert Q(P(t(1, 64, 96)), 0, P(t(1, 128, 96)), 0, 0, P(out)) == 2      # MXFP8
     nt = t(0, 64, 128)
     nt.codes_t, nt.scales_t = None, None
-    assert L.q2d_gemm_quantized(P(a), 0, P(b), 0, 0, P(nt), None) == 1             # both orientations needed
-    assert L.q2d_gemm_quantized(P(a), 0, P(b), 1, 0, P(out), None) == 1            # K mismatch
+    assert Q(P(a), 0, P(b), 0, 0, P(nt)) == 1                              # both orientations needed
+    assert Q(P(a), 0, P(b), 1, 0, P(out)) == 1                             # K mismatch
 
 
 def test_dequantize_error_paths(q2d):

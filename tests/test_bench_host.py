@@ -24,6 +24,10 @@ P = "void q2d::(anonymous namespace)::"
      "gemm_fp4_grouped_k"),
     (P + "gemm_fp4_persistent_kernel<false, false, 0, 1, true>(q2d::GemmArgs, int, int, q2d::GroupedArgs)",
      "gemm_fp4_yq"),
+    (P + "gemm_fp4_persistent_kernel<false, false, 0, 0, true, false>(q2d::GemmArgs, int, int, q2d::GroupedArgs)",
+     "gemm_fp4_yq"),
+    (P + "gemm_fp4_persistent_kernel<false, false, 0, 0, true, true>(q2d::GemmArgs, int, int, q2d::GroupedArgs)",
+     "gemm_fp4_dxq"),
     (P + "gemm_fp8_256_kernel<true, false>(q2d::GemmArgs, int, int)", "gemm_fp8"),
     (P + "gemm_kernel<0, true>(q2d::GemmArgs, long, long)", "gemm_fp4"),
     (P + "gemm_kernel<1, false>(q2d::GemmArgs, long, long)", "gemm_fp8"),
