@@ -616,13 +616,9 @@ __device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &
             float v[16];
 #pragma unroll
             for (int r = 0; r < 16; ++r) v[r] = value(i, j, r);
-            // SR draws (<< 16) of the lane's elements (rows 8 (r / 4) + 4 h + r % 4, column
-            // col), read from the wave's table where a conversion needs them
-            const int cofs = 16 * (col >> 3) + 4 * ((col & 7) >> 1) + 2 * (col & 1);
-            auto rr = [&](int r) __attribute__((always_inline)) -> uint32_t {
-                const int rl = 8 * (r >> 2) + 4 * h + (r & 3);
-                return (uint32_t)*reinterpret_cast<const uint16_t *>(ptab + rl * kPRow + cofs) << 16;
-            };
+            // SR draws of the lane's elements (rows 8 (r / 4) + 4 h + r % 4, column col),
+            // packed two to a register: rw[k] = draw(2k) | draw(2k + 1) << 16
+            uint32_t rw[8];
             if constexpr (SR) {
                 // the previous tile's reads of the table come first (in program order)
                 __builtin_amdgcn_wave_barrier();
@@ -636,10 +632,23 @@ __device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &
                                   (uint32_t)(g.offset >> 32), (uint32_t)g.seed, (uint32_t)(g.seed >> 32), w);
                     *reinterpret_cast<uint4 *>(ptab + brow * kPRow + 16 * bcg) = make_uint4(w[0], w[1], w[2], w[3]);
                 }
-                // LDS accesses of one wave complete in order: the reads below see the table
+                // LDS accesses of one wave complete in order: the reads below see the table.
+                // All 16 reads issue back to back, so their latency is paid once.
                 __builtin_amdgcn_wave_barrier();
                 __builtin_amdgcn_sched_barrier(0);
+                const uint8_t *cp = ptab + 16 * (col >> 3) + 4 * ((col & 7) >> 1) + 2 * (col & 1);
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const int rl = 8 * (k >> 1) + 4 * h + 2 * (k & 1);        // row of element 2k
+                    const uint32_t d0 = *reinterpret_cast<const uint16_t *>(cp + rl * kPRow);
+                    const uint32_t d1 = *reinterpret_cast<const uint16_t *>(cp + (rl + 1) * kPRow);
+                    rw[k] = d0 | (d1 << 16);
+                }
             }
+            // the draw of element r, shifted to bits 31..16
+            auto rr = [&](int r) __attribute__((always_inline)) -> uint32_t {
+                return (r & 1) ? (rw[r >> 1] & 0xFFFF0000u) : (rw[r >> 1] << 16);
+            };
             // column-packed: word q/2 byte 2 (q % 2) + k holds rows (8q + 4h + 2k, +1)
             uint32_t w0 = 0, w1 = 0;
             if constexpr (SR) {
