@@ -295,7 +295,7 @@ class Step:
                     qdx = q2d.QTensor(q2d.FP4_2D, T, K, dev)
                     qb = quant_bytes(dX)
                     off = 100 + len(self.ops)
-                    self.ops.append(("quant_fp4", "%s.dX" % lin.name, qb, qb,
+                    self.ops.append(("quant_fp4", "%s.dX_q" % lin.name, qb, qb,
                                      lambda dX=dX, q=qdx, off=off: q2d.q2d_quantize(dX, "sr", w.seed, off, out=q)))
         self.flops = float(w.gemm_flops)
 

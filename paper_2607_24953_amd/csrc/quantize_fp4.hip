@@ -100,6 +100,49 @@ __device__ __forceinline__ uint32_t sr_pair(int sel, f2v v, uint32_t seed, float
     }
 }
 
+// Stochastic E2M1 conversion of the pair (columns 2k, 2k+1) of one sub-block
+// row into byte `sel` (bf16 rows are one packed register, float32 rows two bit
+// patterns).  Both go through the float32 conversion: the bf16-source form
+// rounds differently near the carry boundary (its parity against the rounding
+// contract fails), so bf16 pairs are widened first.  As for sr_pair, the other
+// bytes of the result are not defined.
+template <typename T>
+__device__ __forceinline__ uint32_t sr_row_pair(int sel, const uint32_t *row, uint32_t seed, float scale)
+{
+    f2v p;
+    if constexpr (sizeof(T) == 2) p = f2v{bits_f(row[sel] << 16), bits_f(row[sel] & 0xFFFF0000u)};
+    else p = f2v{bits_f(row[2 * sel]), bits_f(row[2 * sel + 1])};
+    return sr_pair(sel, p, seed, scale);
+}
+
+// 8 x 8 transpose of 4-bit elements: nibble j of in[i] becomes nibble i of
+// out[j].  Three exchange stages of doubling width (nibbles within row pairs,
+// bytes across distance 2, half-words across distance 4).
+__device__ __forceinline__ void nibble_transpose8(const uint32_t in[8], uint32_t out[8])
+{
+    uint32_t m[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) m[i] = in[i];
+#pragma unroll
+    for (int p = 0; p < 8; p += 2) {
+        const uint32_t t = ((m[p] >> 4) ^ m[p + 1]) & 0x0F0F0F0Fu;
+        m[p + 1] ^= t;
+        m[p] ^= t << 4;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; i += (i & 1) ? 3 : 1) {         // 0, 1, 4, 5
+        const uint32_t x = m[i], y = m[i + 2];
+        m[i] = __builtin_amdgcn_perm(y, x, 0x06020400u);     // bytes x0 y0 x2 y2
+        m[i + 2] = __builtin_amdgcn_perm(y, x, 0x07030501u); // bytes x1 y1 x3 y3
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t x = m[i], y = m[i + 4];
+        out[i] = __builtin_amdgcn_perm(y, x, 0x05040100u);       // x.lo, y.lo
+        out[i + 4] = __builtin_amdgcn_perm(y, x, 0x07060302u);   // x.hi, y.hi
+    }
+}
+
 // Philox4x32-10 block with one 32x32->64 multiply per product (v_mad_u64_u32)
 // and one three-input xor per output word.
 __device__ __forceinline__ void philox_block(uint64_t g, uint32_t o0, uint32_t o1, uint32_t k0, uint32_t k1,
@@ -336,67 +379,94 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
     } else {
         const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
         const uint32_t o0 = (uint32_t)a.offset, o1 = (uint32_t)(a.offset >> 32);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) { rowp[i] = 0; colp[i] = 0; }
-        int64_t idx0 = a.index_base + r0 * a.stride_r + c0;
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            // draws of rows 2m and 2m+1 as seeds r16 << 16
-            uint32_t s16[2][8];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int i = 2 * m + h;
-                uint32_t w[4] = {0, 0, 0, 0}, w2[4] = {0, 0, 0, 0};
-                if (VEC) {
-                    philox_block((uint64_t)idx0 >> 3, o0, o1, k0, k1, w);
-                    if (!ALIGNED8) philox_block(((uint64_t)idx0 >> 3) + 1, o0, o1, k0, k1, w2);
-                }
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    uint32_t r;
-                    if (VEC) {
-                        if (ALIGNED8) {
-                            r = (j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16);
-                        } else {
-                            // the row's eight draws straddle two Philox blocks
-                            const uint32_t q = (uint32_t)(idx0 & 7) + (uint32_t)j;     // 0..14
-                            const uint32_t sq = q & 7u;
-                            const uint32_t wa = (sq & 4u) ? ((sq & 2u) ? w[3] : w[2]) : ((sq & 2u) ? w[1] : w[0]);
-                            const uint32_t wb = (sq & 4u) ? ((sq & 2u) ? w2[3] : w2[2]) : ((sq & 2u) ? w2[1] : w2[0]);
-                            const uint32_t ww = q < 8u ? wa : wb;
-                            r = (sq & 1u) ? (ww & 0xFFFF0000u) : (ww << 16);
-                        }
-                    } else {
-                        const uint64_t idx = (uint64_t)(a.index_base + (r0 + i) * a.stride_r + (c0 + j) * a.stride_c);
-                        r = sr_draw(idx, k0, k1, o0, o1) << 16;
-                    }
-                    s16[h][j] = r;
-                }
-                idx0 += a.stride_r;
+        // the draws of row i (storage index idx_row of its first element) as
+        // seeds r16 << 16
+        auto row_draws = [&](int i, int64_t idx_row, uint32_t s16[8]) __attribute__((always_inline)) {
+            uint32_t w[4] = {0, 0, 0, 0}, w2[4] = {0, 0, 0, 0};
+            if (VEC) {
+                philox_block((uint64_t)idx_row >> 3, o0, o1, k0, k1, w);
+                if (!ALIGNED8) philox_block(((uint64_t)idx_row >> 3) + 1, o0, o1, k0, k1, w2);
             }
-            // rows 2m and 2m+1: pairs (2k, 2k+1) into byte k
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int i = 2 * m + h;
-                const float sc = rscale(i);
-                uint32_t acc = 0;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const f2v pr = {bits_f(elem(i, 2 * k)), bits_f(elem(i, 2 * k + 1))};
-                    const uint32_t lo = sr_pair(k, pr, s16[h][2 * k], sc);
-                    const uint32_t hi = sr_pair(k, pr, s16[h][2 * k + 1] >> 1, sc);
-                    acc |= (lo & (0x0Fu << (8 * k))) | (hi & (0xF0u << (8 * k)));
-                }
-                rowp[i] = acc;
-            }
-            // every column: rows (2m, 2m+1) into byte m
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                const f2v pr = {bits_f(elem(2 * m, j)), bits_f(elem(2 * m + 1, j))};
-                const float sc = cscale(j);
-                const uint32_t lo = sr_pair(m, pr, s16[0][j], sc);
-                const uint32_t hi = sr_pair(m, pr, s16[1][j] >> 1, sc);
-                colp[j] |= (lo & (0x0Fu << (8 * m))) | (hi & (0xF0u << (8 * m)));
+                uint32_t r;
+                if (VEC) {
+                    if (ALIGNED8) {
+                        r = (j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16);
+                    } else {
+                        // the row's eight draws straddle two Philox blocks
+                        const uint32_t q = (uint32_t)(idx_row & 7) + (uint32_t)j;     // 0..14
+                        const uint32_t sq = q & 7u;
+                        const uint32_t wa = (sq & 4u) ? ((sq & 2u) ? w[3] : w[2]) : ((sq & 2u) ? w[1] : w[0]);
+                        const uint32_t wb = (sq & 4u) ? ((sq & 2u) ? w2[3] : w2[2]) : ((sq & 2u) ? w2[1] : w2[0]);
+                        const uint32_t ww = q < 8u ? wa : wb;
+                        r = (sq & 1u) ? (ww & 0xFFFF0000u) : (ww << 16);
+                    }
+                } else {
+                    const uint64_t idx = (uint64_t)(a.index_base + (r0 + i) * a.stride_r + (c0 + j) * a.stride_c);
+                    r = sr_draw(idx, k0, k1, o0, o1) << 16;
+                }
+                s16[j] = r;
+            }
+        };
+        int64_t idx0 = a.index_base + r0 * a.stride_r + c0;
+        if constexpr (!ONED) {
+            // 2D blocks: both layouts share the block scale, so every element is
+            // converted once, row by row; the column-packed words are the 8 x 8
+            // nibble transpose of the row-packed ones
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                uint32_t s16[8];
+                row_draws(i, idx0, s16);
+                idx0 += a.stride_r;
+                uint32_t w = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    // element 2k from a conversion with its draw, element 2k + 1 from
+                    // one with its own (the second element reads seed << 1)
+                    const uint32_t lo = sr_row_pair<T>(k, v[i], s16[2 * k], scale);
+                    const uint32_t hi = sr_row_pair<T>(k, v[i], s16[2 * k + 1] >> 1, scale);
+                    w |= ((lo & 0x0F0F0F0Fu) | (hi & 0xF0F0F0F0u)) & (0xFFu << (8 * k));
+                }
+                rowp[i] = w;
+            }
+            nibble_transpose8(rowp, colp);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) { rowp[i] = 0; colp[i] = 0; }
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                // draws of rows 2m and 2m+1 as seeds r16 << 16
+                uint32_t s16[2][8];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    row_draws(2 * m + h, idx0, s16[h]);
+                    idx0 += a.stride_r;
+                }
+                // rows 2m and 2m+1: pairs (2k, 2k+1) into byte k
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int i = 2 * m + h;
+                    const float sc = rscale(i);
+                    uint32_t acc = 0;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const f2v pr = {bits_f(elem(i, 2 * k)), bits_f(elem(i, 2 * k + 1))};
+                        const uint32_t lo = sr_pair(k, pr, s16[h][2 * k], sc);
+                        const uint32_t hi = sr_pair(k, pr, s16[h][2 * k + 1] >> 1, sc);
+                        acc |= (lo & (0x0Fu << (8 * k))) | (hi & (0xF0u << (8 * k)));
+                    }
+                    rowp[i] = acc;
+                }
+                // every column: rows (2m, 2m+1) into byte m, each with its column's scale
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const f2v pr = {bits_f(elem(2 * m, j)), bits_f(elem(2 * m + 1, j))};
+                    const float sc = cscale(j);
+                    const uint32_t lo = sr_pair(m, pr, s16[0][j], sc);
+                    const uint32_t hi = sr_pair(m, pr, s16[1][j] >> 1, sc);
+                    colp[j] |= (lo & (0x0Fu << (8 * m))) | (hi & (0xF0u << (8 * m)));
+                }
             }
         }
     }
