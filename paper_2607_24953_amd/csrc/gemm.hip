@@ -1007,20 +1007,32 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
 // Large-tile MXFP8 kernel (the query/key projections): 256 x 256 output tile,
 // 4 waves of 128 x 128, E4M3 operands (8 VGPRs per lane per MFMA, 64 cycles
 // each).  A stage holds one K-tile of 64 values: 64 bytes per row of A and of B
-// (16 KB each) and the rows' scale words (the 4-byte word holding this
-// K-tile's two 1x32 scales; 1 KB each), filled by global_load_lds DMA through
-// a ring of kStages stages.  Each iteration runs the 16 MFMAs of one K-tile
-// while the next K-tile's fragments are read and the stage just consumed is
-// refilled; the fragment buffers alternate between two register sets.
-constexpr int kDma8 = 10;                 // per wave per K-tile: 4 A, 4 B, 1 A-scale, 1 B-scale
-constexpr int kStage8 = 2 * kCodeBytes + 2048;
+// (16 KB each), filled by global_load_lds DMA through a ring of kStages
+// stages.  Each iteration runs the 16 MFMAs of one K-tile while the next
+// K-tile's fragments are read and the stage just consumed is refilled; the
+// fragment buffers alternate between two register sets.
+//
+// Scales: a row's 4-byte word holds the 1x32 scales of two K-tiles of 64, and
+// the rows of a tile are ld_scales apart, so a wave's scale load touches one
+// line per lane; those loads, not the codes, bound the first version of this
+// kernel (without them it ran 27-30 % faster).  S16: each row's 16 bytes for
+// eight K-tiles (one group) arrive in one load per operand and wave, into a
+// double-buffered side area of the LDS, issued with the codes of the group's
+// first K-tile; the last group's load is shifted back to end at the row's last
+// word.  Otherwise (K below 512, or rows of scales not 16-byte aligned) the
+// word of an even K-tile goes into its stage and the odd K-tile reuses it.
+constexpr int kDma8Codes = 8;                   // per wave per K-tile: 4 A and 4 B code loads
+constexpr int kStage8 = 2 * kCodeBytes + 2048;  // word path: codes, then the A and B words
+constexpr int kSide8 = 2 * 2 * 256 * 16;        // S16: 2 groups x {A, B} x 256 rows x 16 bytes
 
-template <bool BF16OUT, bool ACC>
+template <bool BF16OUT, bool ACC, bool S16>
 __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, int tiles_m, int tiles_n)
 {
     using F = Fmt<kFmtMxfp8>;
     constexpr int RB = 64;                          // bytes per row per K-tile of 64
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStage8];
+    constexpr int kStageB = S16 ? 2 * kCodeBytes : kStage8;
+    constexpr int kSide = kStages * kStageB;        // S16 side area
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageB + (S16 ? kSide8 : 0)];
 
     int tm, tn;
     {
@@ -1034,11 +1046,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
     const int wm = wave >> 1, wn = wave & 1;
     const int half = lane >> 5;
     const uint32_t nk = (uint32_t)(g.K / 64);       // K is a multiple of 128
+    const uint32_t nw = (uint32_t)(g.K / 128);      // scale words per row (S16: at least 4)
 
     // codes: DMA j of this wave fills bytes [(4j + wave) * 1024, +1024) of an
     // operand stage (rows 16 (4j + wave) + lane / 4, physical chunk lane % 4,
     // the 64-byte-row swizzle of the E2M1 kernel); scales: the wave's DMA
-    // fills rows 64 wave + lane of the stage's A and B scale words
+    // covers rows 64 wave + lane of the tile's A and B rows
     uint32_t offA[4], offB[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -1049,19 +1062,23 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
         offA[j] = (uint32_t)(ra * g.lda + c * 16);
         offB[j] = (uint32_t)(rb * g.ldb + c * 16);
     }
-    const uint8_t *srcSA, *srcSB;
+    uint32_t soffA, soffB;
     {
         int64_t ra = m0 + 64 * wave + lane; ra = ra < g.M ? ra : g.M - 1;
         int64_t rb = n0 + 64 * wave + lane; rb = rb < g.N ? rb : g.N - 1;
-        srcSA = g.sa + ra * g.ldsa;
-        srcSB = g.sb + rb * g.ldsb;
+        soffA = (uint32_t)(ra * g.ldsa);
+        soffB = (uint32_t)(rb * g.ldsb);
     }
     const uint32_t lds0 = (uint32_t)(uintptr_t)&smem[0];
     const int sw = Fmt<kFmtFp4Block2D>::swz(lane & 31);
     const int rd_a = (wm * 128 + (lane & 31)) * RB;
     const int rd_b = kCodeBytes + (wn * 128 + (lane & 31)) * RB;
-    const int rs_a = 2 * kCodeBytes + (wm * 128 + (lane & 31)) * 4;
-    const int rs_b = 2 * kCodeBytes + 1024 + (wn * 128 + (lane & 31)) * 4;
+    // the lane's row words: word path at stage + 2 * kCodeBytes (+ 1024 for B);
+    // S16 at side + group buffer * 8192 (+ 4096 for B) + 16 * row
+    const int rs_a = S16 ? kSide + (wm * 128 + (lane & 31)) * 16 : 2 * kCodeBytes + (wm * 128 + (lane & 31)) * 4;
+    const int rs_b = S16 ? kSide + 4096 + (wn * 128 + (lane & 31)) * 16
+                         : 2 * kCodeBytes + 1024 + (wn * 128 + (lane & 31)) * 4;
+    constexpr int kRowStride = S16 ? 32 * 16 : 32 * 4;      // words of fragment tile i + 1
 
     v16f acc[4][4];
 #pragma unroll
@@ -1071,24 +1088,54 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    auto dma = [&](uint32_t t, int part) {          // part 0..9
+    // code loads of K-tile t (part 0..7); past the last K-tile they repeat it
+    // into a stage that is never read
+    auto dma = [&](uint32_t t, int part) __attribute__((always_inline)) {
         const uint32_t tt = t < nk ? t : nk - 1;
-        const uint32_t stage = lds0 + (t % kStages) * kStage8;
-        if (part < 8) {
-            const int jj = part >> 1;
-            if ((part & 1) == 0) lds_dma16(g.a + tt * RB, offA[jj], stage + (4 * jj + wave) * 1024);
-            else lds_dma16(g.b + tt * RB, offB[jj], stage + kCodeBytes + (4 * jj + wave) * 1024);
-        } else if (part == 8) {
-            lds_dma4(srcSA + (tt >> 1) * 4, stage + 2 * kCodeBytes + wave * 256);
+        const uint32_t stage = lds0 + (t % kStages) * kStageB;
+        const int jj = part >> 1;
+        if ((part & 1) == 0) lds_dma16(g.a + tt * RB, offA[jj], stage + (4 * jj + wave) * 1024);
+        else lds_dma16(g.b + tt * RB, offB[jj], stage + kCodeBytes + (4 * jj + wave) * 1024);
+    };
+    // scale loads: word path, the word of even K-tile t into its stage; S16, the
+    // 16 bytes of group p (shifted back for the last group) into buffer p & 1
+    auto sdma = [&](uint32_t t) __attribute__((always_inline)) {
+        if constexpr (S16) {
+            const uint32_t p = t >> 3;
+            const uint32_t o = 4 * (4 * p < nw - 4 ? 4 * p : nw - 4);
+            const uint32_t buf = lds0 + kSide + (p & 1) * 8192;
+            lds_dma16(g.sa, soffA + o, buf + wave * 1024);
+            lds_dma16(g.sb, soffB + o, buf + 4096 + wave * 1024);
         } else {
-            lds_dma4(srcSB + (tt >> 1) * 4, stage + 2 * kCodeBytes + 1024 + wave * 256);
+            const uint32_t tt = t < nk ? t : nk - 1;
+            const uint32_t stage = lds0 + (t % kStages) * kStageB;
+            lds_dma4(g.sa + soffA + (tt >> 1) * 4, stage + 2 * kCodeBytes + wave * 256);
+            lds_dma4(g.sb + soffB + (tt >> 1) * 4, stage + 2 * kCodeBytes + 1024 + wave * 256);
         }
     };
+    // does K-tile t bring scale loads with it
+    auto has_scales = [&](uint32_t t) __attribute__((always_inline)) -> bool {
+        return S16 ? (t & 7) == 0 : (t & 1) == 0;
+    };
+    // LDS address of the word of even K-tile t for fragment row base `rs`
+    auto word_at = [&](uint32_t t, int rs) __attribute__((always_inline)) -> const uint32_t * {
+        if constexpr (S16) {
+            const uint32_t p = t >> 3;
+            uint32_t w = (t >> 1) - (4 * p < nw - 4 ? 4 * p : nw - 4);
+            w = w < 3 ? w : 3;                      // K-tile nk (read, never used) stays in the row's slot
+            return reinterpret_cast<const uint32_t *>(smem + rs + (p & 1) * 8192 + 4 * w);
+        } else {
+            return reinterpret_cast<const uint32_t *>(smem + (t % kStages) * kStageB + rs);
+        }
+    };
+
     // fragments of one K-tile: A tile i / B tile j as two 16-byte chunks
-    // (chunks half and 2 + half of the row) and the rows' scale words; each
-    // is re-read from the next K-tile's stage right after its last use
-    v8i fa[4], fb[4];
-    uint32_t sa[4], sb[4];
+    // (chunks half and 2 + half of the row) and the rows' scale words, in two
+    // register sets: while one K-tile's MFMAs run on one set, the next
+    // K-tile's fragments are read into the other early in the K-tile, so the
+    // reads have landed long before their first use
+    v8i fa0[4], fb0[4], fa1[4], fb1[4];
+    uint32_t sa0[4], sb0[4], sa1[4], sb1[4];
     const int c0 = (half ^ sw) * 16, c1 = ((2 + half) ^ sw) * 16;
 #define Q2D_RD8(dst, base, row_off)                                                                  \
     do {                                                                                             \
@@ -1098,49 +1145,73 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
         dst[4] = (int)x1_.x; dst[5] = (int)x1_.y; dst[6] = (int)x1_.z; dst[7] = (int)x1_.w;          \
     } while (0)
 
+    // K-tile kt (odd when ODD) on (fa, fb, sa, sb); the fragments of K-tile kt + 1
+    // into (na, nb, nsa, nsb)
+    auto ktile = [&](auto odd, uint32_t kt, v8i (&fa)[4], v8i (&fb)[4], uint32_t (&sa)[4], uint32_t (&sb)[4],
+                     v8i (&na)[4], v8i (&nb)[4], uint32_t (&nsa)[4], uint32_t (&nsb)[4]) __attribute__((always_inline)) {
+        constexpr bool ODD = decltype(odd)::value;
+        __builtin_amdgcn_s_waitcnt(0xC07F);                     // lgkmcnt(0): this K-tile's reads done
+        // K-tile kt + 1 and its scales landed: at most the code loads of kt + 2 and
+        // kt + 3 outstanding (when scale loads came with those, this also waits
+        // for some of them, which is only early)
+        wait_vmcnt<2 * kDma8Codes>();
+        block_barrier();
+        const uint8_t *sn = smem + ((kt + 1) % kStages) * kStageB;   // past the last K-tile: unused reads
+        const int byte = 2 * (kt & 1) + half;                   // this K-tile's scale in the row word
+        const bool sc_next = has_scales(kt + kStages);          // K-tile kt + 4's loads include scales
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int sa_ = (int)((sa[i] >> (8 * byte)) & 0xFFu);
+                const int sb_ = (int)((sb[j] >> (8 * byte)) & 0xFFu);
+                acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[j], acc[i][j], F::kCbsz,
+                                                                            F::kCbsz, 0, sa_, 0, sb_);
+                __builtin_amdgcn_sched_barrier(0);
+                const int q = 4 * i + j;
+                if (q < kDma8Codes) {
+                    dma(kt + kStages, q);
+                    __builtin_amdgcn_sched_barrier(0);
+                } else if (q == kDma8Codes && sc_next) {
+                    sdma(kt + kStages);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                if (q >= 1 && q <= 8) {
+                    const int f = (q - 1) >> 1;
+                    // an odd K-tile's words are the even one's
+                    if (((q - 1) & 1) == 0) {
+                        Q2D_RD8(na[f], sn, rd_a + f * 32 * RB);
+                        nsa[f] = ODD ? word_at(kt + 1, rs_a + f * kRowStride)[0] : sa[f];
+                    } else {
+                        Q2D_RD8(nb[f], sn, rd_b + f * 32 * RB);
+                        nsb[f] = ODD ? word_at(kt + 1, rs_b + f * kRowStride)[0] : sb[f];
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+        }
+    };
+
     if (nk > 0) {
-        for (int t = 0; t < kStages; ++t)
-            for (int p = 0; p < kDma8; ++p) dma((uint32_t)t, p);
-        wait_vmcnt<(kStages - 1) * kDma8>();
+        for (uint32_t t = 0; t < kStages; ++t) {
+            for (int p = 0; p < kDma8Codes; ++p) dma(t, p);
+            if (has_scales(t)) sdma(t);
+        }
+        // K-tile 0 and its scales landed: the loads of K-tiles 1..3 may be outstanding
+        // (S16: 3 x 8 code loads; word path: 3 x 8 code loads and 2 scale loads)
+        wait_vmcnt<3 * kDma8Codes + (S16 ? 0 : 2)>();
         block_barrier();
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            Q2D_RD8(fa[i], smem, rd_a + i * 32 * RB);
-            Q2D_RD8(fb[i], smem, rd_b + i * 32 * RB);
-            sa[i] = *reinterpret_cast<const uint32_t *>(smem + rs_a + i * 32 * 4);
-            sb[i] = *reinterpret_cast<const uint32_t *>(smem + rs_b + i * 32 * 4);
+            Q2D_RD8(fa0[i], smem, rd_a + i * 32 * RB);
+            Q2D_RD8(fb0[i], smem, rd_b + i * 32 * RB);
+            sa0[i] = word_at(0, rs_a + i * kRowStride)[0];
+            sb0[i] = word_at(0, rs_b + i * kRowStride)[0];
         }
-        for (uint32_t kt = 0; kt < nk; ++kt) {
-            __builtin_amdgcn_s_waitcnt(0xC07F);                 // lgkmcnt(0): this K-tile's reads done
-            wait_vmcnt<(kStages - 2) * kDma8>();                // K-tile kt + 1 landed
-            block_barrier();
-            const uint8_t *sn = smem + ((kt + 1) % kStages) * kStage8;   // past the last K-tile: unused reads
-            const int byte = 2 * (kt & 1) + half;               // this K-tile's scale in the row word
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int sa_ = (int)((sa[i] >> (8 * byte)) & 0xFFu);
-                    const int sb_ = (int)((sb[j] >> (8 * byte)) & 0xFFu);
-                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[i], fb[j], acc[i][j],
-                                                                                F::kCbsz, F::kCbsz, 0, sa_, 0, sb_);
-                    __builtin_amdgcn_sched_barrier(0);
-                    const int q = 4 * i + j;
-                    if (q < 10) {
-                        dma(kt + kStages, q);
-                        __builtin_amdgcn_sched_barrier(0);
-                    }
-                    if (i == 3) {                               // last use of B tile j
-                        Q2D_RD8(fb[j], sn, rd_b + j * 32 * RB);
-                        sb[j] = *reinterpret_cast<const uint32_t *>(sn + rs_b + j * 32 * 4);
-                        __builtin_amdgcn_sched_barrier(0);
-                    }
-                }
-                // last use of A tile i
-                Q2D_RD8(fa[i], sn, rd_a + i * 32 * RB);
-                sa[i] = *reinterpret_cast<const uint32_t *>(sn + rs_a + i * 32 * 4);
-                __builtin_amdgcn_sched_barrier(0);
-            }
+        // nk is even (K is a multiple of 128)
+        for (uint32_t kt = 0; kt < nk; kt += 2) {
+            ktile(std::false_type{}, kt, fa0, fb0, sa0, sb0, fa1, fb1, sa1, sb1);
+            ktile(std::true_type{}, kt + 1, fa1, fb1, sa1, sb1, fa0, fb0, sa0, sb0);
         }
         wait_vmcnt<0>();
     }
@@ -1211,12 +1282,26 @@ hipError_t launch_gemm(const GemmArgs &g, int fmt, int c_is_bf16, hipStream_t st
         return c_is_bf16 ? launch_t<kFmtFp4Block2D, true>(g, stream) : launch_t<kFmtFp4Block2D, false>(g, stream);
     if (off32 && ((g.M + BM2 - 1) / BM2) * ((g.N + BN2 - 1) / BN2) >= 128) {
         const int tm = (int)((g.M + BM2 - 1) / BM2), tn = (int)((g.N + BN2 - 1) / BN2);
-        if (c_is_bf16) {
-            if (g.accumulate) hipLaunchKernelGGL((gemm_fp8_256_kernel<true, true>), dim3(tm * tn), dim3(kThreads), 0, stream, g, tm, tn);
-            else hipLaunchKernelGGL((gemm_fp8_256_kernel<true, false>), dim3(tm * tn), dim3(kThreads), 0, stream, g, tm, tn);
+        // 16-byte scale loads: at least one group of 8 K-tiles, 16-byte aligned rows
+        const bool s16 = g.K >= 512 && g.ldsa % 16 == 0 && g.ldsb % 16 == 0 &&
+                         reinterpret_cast<uintptr_t>(g.sa) % 16 == 0 && reinterpret_cast<uintptr_t>(g.sb) % 16 == 0;
+        const dim3 grid((unsigned)(tm * tn)), block(kThreads);
+        if (s16) {
+            if (c_is_bf16) {
+                if (g.accumulate) hipLaunchKernelGGL((gemm_fp8_256_kernel<true, true, true>), grid, block, 0, stream, g, tm, tn);
+                else hipLaunchKernelGGL((gemm_fp8_256_kernel<true, false, true>), grid, block, 0, stream, g, tm, tn);
+            } else {
+                if (g.accumulate) hipLaunchKernelGGL((gemm_fp8_256_kernel<false, true, true>), grid, block, 0, stream, g, tm, tn);
+                else hipLaunchKernelGGL((gemm_fp8_256_kernel<false, false, true>), grid, block, 0, stream, g, tm, tn);
+            }
         } else {
-            if (g.accumulate) hipLaunchKernelGGL((gemm_fp8_256_kernel<false, true>), dim3(tm * tn), dim3(kThreads), 0, stream, g, tm, tn);
-            else hipLaunchKernelGGL((gemm_fp8_256_kernel<false, false>), dim3(tm * tn), dim3(kThreads), 0, stream, g, tm, tn);
+            if (c_is_bf16) {
+                if (g.accumulate) hipLaunchKernelGGL((gemm_fp8_256_kernel<true, true, false>), grid, block, 0, stream, g, tm, tn);
+                else hipLaunchKernelGGL((gemm_fp8_256_kernel<true, false, false>), grid, block, 0, stream, g, tm, tn);
+            } else {
+                if (g.accumulate) hipLaunchKernelGGL((gemm_fp8_256_kernel<false, true, false>), grid, block, 0, stream, g, tm, tn);
+                else hipLaunchKernelGGL((gemm_fp8_256_kernel<false, false, false>), grid, block, 0, stream, g, tm, tn);
+            }
         }
         return hipGetLastError();
     }

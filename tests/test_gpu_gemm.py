@@ -194,8 +194,11 @@ def test_linear_fwd_bwd(q2d, T, N, K):
 
 @pytest.mark.parametrize("M,N,K", [(128, 256, 256), (300, 200, 160), (1000, 300, 2000),
                                    # enough 256 x 256 tiles for the large-tile kernel: ragged
-                                   # edges, K shorter than its 4-stage ring (256 = 4 K-tiles of 64)
-                                   (4096, 2048, 1024), (4000, 2100, 640), (2048, 4224, 256)])
+                                   # edges, K shorter than its 4-stage ring (256 = 4 K-tiles of 64);
+                                   # 16-byte scale groups of 8 K-tiles for K = 1024 and 1536 (an
+                                   # odd number of groups), per-word scales for K = 640 and 256
+                                   (4096, 2048, 1024), (4096, 2304, 1536), (4000, 2100, 640),
+                                   (2048, 4224, 256)])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 1), (1, 0)])
 @pytest.mark.parametrize("data", ["normal", "adversarial"])
 def test_gemm_mxfp8(q2d, M, N, K, ta, tb, data):
