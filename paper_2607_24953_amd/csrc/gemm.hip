@@ -1018,9 +1018,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
 // kernel (without them it ran 27-30 % faster).  S16: each row's 16 bytes for
 // eight K-tiles (one group) arrive in one load per operand and wave, into a
 // double-buffered side area of the LDS, issued with the codes of the group's
-// first K-tile; the last group's load is shifted back to end at the row's last
-// word.  Otherwise (K below 512, or rows of scales not 16-byte aligned) the
-// word of an even K-tile goes into its stage and the odd K-tile reuses it.
+// first K-tile.  Otherwise (K not a multiple of 512, or rows of scales not
+// 16-byte aligned) the word of an even K-tile goes into its stage and the odd
+// K-tile reuses it.
 constexpr int kDma8Codes = 8;                   // per wave per K-tile: 4 A and 4 B code loads
 constexpr int kStage8 = 2 * kCodeBytes + 2048;  // word path: codes, then the A and B words
 constexpr int kSide8 = 2 * 2 * 256 * 16;        // S16: 2 groups x {A, B} x 256 rows x 16 bytes
@@ -1098,7 +1098,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
         else lds_dma16(g.b + tt * RB, offB[jj], stage + kCodeBytes + (4 * jj + wave) * 1024);
     };
     // scale loads: word path, the word of even K-tile t into its stage; S16, the
-    // 16 bytes of group p (shifted back for the last group) into buffer p & 1
+    // 16 bytes of group p into buffer p & 1 (past the last group, the last one's
+    // bytes again: those loads fill a buffer that is never read)
     auto sdma = [&](uint32_t t) __attribute__((always_inline)) {
         if constexpr (S16) {
             const uint32_t p = t >> 3;
@@ -1145,20 +1146,22 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
         dst[4] = (int)x1_.x; dst[5] = (int)x1_.y; dst[6] = (int)x1_.z; dst[7] = (int)x1_.w;          \
     } while (0)
 
-    // K-tile kt (odd when ODD) on (fa, fb, sa, sb); the fragments of K-tile kt + 1
-    // into (na, nb, nsa, nsb)
-    auto ktile = [&](auto odd, uint32_t kt, v8i (&fa)[4], v8i (&fb)[4], uint32_t (&sa)[4], uint32_t (&sb)[4],
+    // K-tile kt on (fa, fb, sa, sb); the fragments of K-tile kt + 1 into (na, nb,
+    // nsa, nsb).  PH = kt mod 8 (S16) or kt mod 2: which K-tiles around kt carry
+    // scale loads, so the waits count exactly the loads that may stay outstanding
+    auto ktile = [&](auto ph, uint32_t kt, v8i (&fa)[4], v8i (&fb)[4], uint32_t (&sa)[4], uint32_t (&sb)[4],
                      v8i (&na)[4], v8i (&nb)[4], uint32_t (&nsa)[4], uint32_t (&nsb)[4]) __attribute__((always_inline)) {
-        constexpr bool ODD = decltype(odd)::value;
+        constexpr int PH = decltype(ph)::value;
+        constexpr bool ODD = (PH & 1) != 0;
+        constexpr auto scales_at = [](int t) { return S16 ? (t & 7) == 0 : (t & 1) == 0; };
+        // K-tile kt + 1 and its scales landed: the loads of kt + 2 and kt + 3 may not have
+        constexpr int kAfter = 2 * kDma8Codes + (scales_at(PH + 2) ? 2 : 0) + (scales_at(PH + 3) ? 2 : 0);
+        constexpr bool kScNext = scales_at(PH + kStages);       // K-tile kt + 4's loads include scales
         __builtin_amdgcn_s_waitcnt(0xC07F);                     // lgkmcnt(0): this K-tile's reads done
-        // K-tile kt + 1 and its scales landed: at most the code loads of kt + 2 and
-        // kt + 3 outstanding (when scale loads came with those, this also waits
-        // for some of them, which is only early)
-        wait_vmcnt<2 * kDma8Codes>();
+        wait_vmcnt<kAfter>();
         block_barrier();
         const uint8_t *sn = smem + ((kt + 1) % kStages) * kStageB;   // past the last K-tile: unused reads
         const int byte = 2 * (kt & 1) + half;                   // this K-tile's scale in the row word
-        const bool sc_next = has_scales(kt + kStages);          // K-tile kt + 4's loads include scales
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -1172,7 +1175,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
                 if (q < kDma8Codes) {
                     dma(kt + kStages, q);
                     __builtin_amdgcn_sched_barrier(0);
-                } else if (q == kDma8Codes && sc_next) {
+                } else if (q == kDma8Codes && kScNext) {
                     sdma(kt + kStages);
                     __builtin_amdgcn_sched_barrier(0);
                 }
@@ -1208,10 +1211,25 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
             sa0[i] = word_at(0, rs_a + i * kRowStride)[0];
             sb0[i] = word_at(0, rs_b + i * kRowStride)[0];
         }
-        // nk is even (K is a multiple of 128)
-        for (uint32_t kt = 0; kt < nk; kt += 2) {
-            ktile(std::false_type{}, kt, fa0, fb0, sa0, sb0, fa1, fb1, sa1, sb1);
-            ktile(std::true_type{}, kt + 1, fa1, fb1, sa1, sb1, fa0, fb0, sa0, sb0);
+        using std::integral_constant;
+        if constexpr (S16) {
+            // nk is a multiple of 8 (K of 512)
+            for (uint32_t kt = 0; kt < nk; kt += 8) {
+                ktile(integral_constant<int, 0>{}, kt, fa0, fb0, sa0, sb0, fa1, fb1, sa1, sb1);
+                ktile(integral_constant<int, 1>{}, kt + 1, fa1, fb1, sa1, sb1, fa0, fb0, sa0, sb0);
+                ktile(integral_constant<int, 2>{}, kt + 2, fa0, fb0, sa0, sb0, fa1, fb1, sa1, sb1);
+                ktile(integral_constant<int, 3>{}, kt + 3, fa1, fb1, sa1, sb1, fa0, fb0, sa0, sb0);
+                ktile(integral_constant<int, 4>{}, kt + 4, fa0, fb0, sa0, sb0, fa1, fb1, sa1, sb1);
+                ktile(integral_constant<int, 5>{}, kt + 5, fa1, fb1, sa1, sb1, fa0, fb0, sa0, sb0);
+                ktile(integral_constant<int, 6>{}, kt + 6, fa0, fb0, sa0, sb0, fa1, fb1, sa1, sb1);
+                ktile(integral_constant<int, 7>{}, kt + 7, fa1, fb1, sa1, sb1, fa0, fb0, sa0, sb0);
+            }
+        } else {
+            // nk is even (K is a multiple of 128)
+            for (uint32_t kt = 0; kt < nk; kt += 2) {
+                ktile(integral_constant<int, 0>{}, kt, fa0, fb0, sa0, sb0, fa1, fb1, sa1, sb1);
+                ktile(integral_constant<int, 1>{}, kt + 1, fa1, fb1, sa1, sb1, fa0, fb0, sa0, sb0);
+            }
         }
         wait_vmcnt<0>();
     }
@@ -1282,8 +1300,8 @@ hipError_t launch_gemm(const GemmArgs &g, int fmt, int c_is_bf16, hipStream_t st
         return c_is_bf16 ? launch_t<kFmtFp4Block2D, true>(g, stream) : launch_t<kFmtFp4Block2D, false>(g, stream);
     if (off32 && ((g.M + BM2 - 1) / BM2) * ((g.N + BN2 - 1) / BN2) >= 128) {
         const int tm = (int)((g.M + BM2 - 1) / BM2), tn = (int)((g.N + BN2 - 1) / BN2);
-        // 16-byte scale loads: at least one group of 8 K-tiles, 16-byte aligned rows
-        const bool s16 = g.K >= 512 && g.ldsa % 16 == 0 && g.ldsb % 16 == 0 &&
+        // 16-byte scale loads: whole groups of 8 K-tiles, 16-byte aligned rows
+        const bool s16 = g.K % 512 == 0 && g.ldsa % 16 == 0 && g.ldsb % 16 == 0 &&
                          reinterpret_cast<uintptr_t>(g.sa) % 16 == 0 && reinterpret_cast<uintptr_t>(g.sb) % 16 == 0;
         const dim3 grid((unsigned)(tm * tn)), block(kThreads);
         if (s16) {

@@ -197,6 +197,7 @@ def test_linear_fwd_bwd(q2d, T, N, K):
                                    # edges, K shorter than its 4-stage ring (256 = 4 K-tiles of 64);
                                    # 16-byte scale groups of 8 K-tiles for K = 1024 and 1536 (an
                                    # odd number of groups), per-word scales for K = 640 and 256
+                                   # (not multiples of 512)
                                    (4096, 2048, 1024), (4096, 2304, 1536), (4000, 2100, 640),
                                    (2048, 4224, 256)])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 1), (1, 0)])
