@@ -102,9 +102,49 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-tokens", type=int, default=256)
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    p.add_argument("--hot-loop", default="", choices=["", "gemm", "quant", "quant_sr"],
+                   help="run one kernel of the 7B QKV shape in a loop for --seconds (for sampling "
+                        "power and clocks from outside) and print its rate")
+    p.add_argument("--seconds", type=float, default=8.0)
     p.add_argument("--summarize-profiles", default="", metavar="DIR",
                    help="write profiles/ summaries from the rocprofv3 outputs in DIR")
     return p.parse_args()
+
+
+def hot_loop(torch, kind: str, seconds: float):
+    """One kernel of the 7B QKV projection (16384 x 4096 activations, 12288 x 4096
+    weight) in a loop: the forward FP4 GEMM, or the quantizer of X (round to nearest
+    or stochastic).  Progress goes to stderr, the rate to stdout as one JSON line."""
+    import synth
+    import paper_2607_24953_amd as q2d
+    dev = "cuda:0"
+    X = synth.normal((16384, 4096), 1.0, 7001, torch.bfloat16, dev)
+    W = synth.normal((12288, 4096), 0.02, 7002, torch.bfloat16, dev)
+    qx = q2d.q2d_quantize(X, "rtn", 0, 0)
+    qw = q2d.q2d_quantize(W, "rtn", 0, 1)
+    Y = torch.empty(16384, 12288, dtype=torch.bfloat16, device=dev)
+    calls = {"gemm": lambda: q2d.q2d_gemm(qx, 0, qw, 0, out=Y),
+             "quant": lambda: q2d.q2d_quantize(X, "rtn", 0, 0, out=qx),
+             "quant_sr": lambda: q2d.q2d_quantize(X, "sr", 0, 0, out=qx)}
+    call = calls[kind]
+    for _ in range(3):
+        call()
+    torch.cuda.synchronize()
+    print("hot loop %s: start" % kind, file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    n = 0
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            call()
+        torch.cuda.synchronize()
+        n += 20
+    dt = (time.perf_counter() - t0) / n
+    if kind == "gemm":
+        rate, unit = 2.0 * 16384 * 12288 * 4096 / dt / 1e12, "TFLOP/s"
+    else:
+        rate, unit = 16384 * 4096 * 3.001 / dt / 1e9, "GB/s"
+    print(json.dumps({"hot_loop": kind, "launches": n, "ms_per_launch": round(dt * 1e3, 4),
+                      "rate": round(rate, 1), "unit": unit}), flush=True)
 
 
 def copy_calibration(torch, nbytes: int, reps: int = 3):
@@ -654,6 +694,9 @@ def main():
     import torch
     if args.copy_calibration:
         copy_calibration(torch, args.copy_calibration)
+        return
+    if args.hot_loop:
+        hot_loop(torch, args.hot_loop, args.seconds)
         return
     import synth
     import paper_2607_24953_amd as q2d
