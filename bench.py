@@ -102,7 +102,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-tokens", type=int, default=256)
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
-    p.add_argument("--hot-loop", default="", choices=["", "gemm", "quant", "quant_sr"],
+    p.add_argument("--hot-loop", default="", choices=["", "gemm", "gemm_fp8", "quant", "quant_sr"],
                    help="run one kernel of the 7B QKV shape in a loop for --seconds (for sampling "
                         "power and clocks from outside) and print its rate")
     p.add_argument("--seconds", type=float, default=8.0)
@@ -113,8 +113,8 @@ def parse():
 
 def hot_loop(torch, kind: str, seconds: float):
     """One kernel of the 7B QKV projection (16384 x 4096 activations, 12288 x 4096
-    weight) in a loop: the forward FP4 GEMM, or the quantizer of X (round to nearest
-    or stochastic).  Progress goes to stderr, the rate to stdout as one JSON line."""
+    weight) in a loop: the forward FP4 or MXFP8 GEMM, or the FP4 quantizer of X (round
+    to nearest or stochastic).  Progress goes to stderr, the rate to stdout as one JSON line."""
     import synth
     import paper_2607_24953_amd as q2d
     dev = "cuda:0"
@@ -123,7 +123,11 @@ def hot_loop(torch, kind: str, seconds: float):
     qx = q2d.q2d_quantize(X, "rtn", 0, 0)
     qw = q2d.q2d_quantize(W, "rtn", 0, 1)
     Y = torch.empty(16384, 12288, dtype=torch.bfloat16, device=dev)
+    if kind == "gemm_fp8":
+        qx = q2d.mxfp8_quantize(X)
+        qw = q2d.mxfp8_quantize(W)
     calls = {"gemm": lambda: q2d.q2d_gemm(qx, 0, qw, 0, out=Y),
+             "gemm_fp8": lambda: q2d.q2d_gemm(qx, 0, qw, 0, out=Y),
              "quant": lambda: q2d.q2d_quantize(X, "rtn", 0, 0, out=qx),
              "quant_sr": lambda: q2d.q2d_quantize(X, "sr", 0, 0, out=qx)}
     call = calls[kind]
@@ -139,7 +143,7 @@ def hot_loop(torch, kind: str, seconds: float):
         torch.cuda.synchronize()
         n += 20
     dt = (time.perf_counter() - t0) / n
-    if kind == "gemm":
+    if kind.startswith("gemm"):
         rate, unit = 2.0 * 16384 * 12288 * 4096 / dt / 1e12, "TFLOP/s"
     else:
         rate, unit = 16384 * 4096 * 3.001 / dt / 1e9, "GB/s"
@@ -426,6 +430,15 @@ def measure(step, torch, steps: int, warmup: int) -> dict:
                               "launches_timed": n, "avg_launch_ms": round(ms / n, 5),
                               "work_per_launch": work / n, "algorithmic_bytes_per_launch": abytes / n,
                               "ms_per_step": round(ms / steps, 4)}
+        if bound == "mfma":
+            # both ceilings of a launch: its flops at the MFMA peak and its algorithmic
+            # bytes (operands once, output once) at the HBM peak; a short-K GEMM whose
+            # bf16 output outweighs its flops sits on the HBM side of the ridge
+            t_mfma = work / n / (peak * 1e12)
+            t_hbm = abytes / n / (PEAK_HBM_GBS * 1e9)
+            res["kinds"][kind]["ideal_ms"] = {"mfma": round(t_mfma * 1e3, 5), "hbm": round(t_hbm * 1e3, 5)}
+            res["kinds"][kind]["ridge_side"] = "hbm" if t_hbm > t_mfma else "mfma"
+            res["kinds"][kind]["frac_of_roofline"] = round(max(t_mfma, t_hbm) / (ms / n * 1e-3), 4)
     for name, (kind, ms, work, n) in names.items():
         unit = KIND_PEAK[kind][2]
         rate = work / (ms * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)

@@ -348,7 +348,8 @@ __device__ __forceinline__ void store_tile(v16f (&acc)[4][4], const GemmArgs &g,
 // Persistent FP4 kernel (the large-tile design above).  The grid holds one
 // workgroup per CU, a multiple of the 8 XCDs so that a workgroup keeps its
 // XCD's share of the tile order; each walks the tiles u = blockIdx.x,
-// blockIdx.x + gridDim.x, ...  The K-tiles of all its tiles form one stream
+// blockIdx.x + gridDim.x, ... (ragged K: a serpentine over the tiles sorted by
+// cost, TileSpace::step).  The K-tiles of all its tiles form one stream
 // through the LDS ring: the loads of the next tile's first K-tiles are in
 // flight while the current tile finishes and its accumulators are written, so
 // no tile pays the pipeline fill.  Iteration s of the K loop: (A) the 16 MFMAs
@@ -376,17 +377,34 @@ struct TileSpace {
     uint32_t total;        // tiles (ragged M: row tiles of all experts x column tiles)
     uint32_t per, rem, span;   // dense: XCD share of the tile order, group span
 
+    // Ragged K: u is a position in the tile order sorted by cost, experts by
+    // descending K-tile count (tile_start holds that expert order), each expert's
+    // tiles in row-major order.  A workgroup takes positions G k + w for even k and
+    // G k + G - 1 - w for odd k (G workgroups, w its index): the serpentine over a
+    // descending list keeps the K-tiles per workgroup even when a few experts hold
+    // most of the tokens.
+    __device__ __forceinline__ int32_t expert_at(uint32_t u) const
+    {
+        return __builtin_amdgcn_readfirstlane(tile_start[u / (uint32_t)(tiles_m * tiles_n)]);
+    }
     __device__ __forceinline__ uint32_t nk_of(uint32_t u) const
     {
         if (GMODE != 2) return (uint32_t)(g.K / BK);
-        const uint32_t e = u / (uint32_t)(tiles_m * tiles_n);
+        const int32_t e = expert_at(u);
         return (uint32_t)__builtin_amdgcn_readfirstlane((pad_start[e + 1] - pad_start[e]) / BK);
     }
-    // first tile at or after u (stepping by the grid) with at least one K-tile
+    // the workgroup's next tile after u
+    __device__ __forceinline__ uint32_t step(uint32_t u) const
+    {
+        if (GMODE != 2) return u + gridDim.x;
+        const uint32_t k = u / gridDim.x + 1;
+        return k * gridDim.x + ((k & 1) ? gridDim.x - 1 - blockIdx.x : blockIdx.x);
+    }
+    // u, or past the end if u has no K-tile (ragged K: every later position of
+    // the cost order is empty too)
     __device__ __forceinline__ uint32_t valid_from(uint32_t u) const
     {
-        if (GMODE == 2)
-            while (u < total && nk_of(u) == 0) u += gridDim.x;
+        if (GMODE == 2 && u < total && nk_of(u) == 0) return total;
         return u;
     }
     __device__ __forceinline__ TileRef ref(uint32_t u) const
@@ -427,8 +445,8 @@ struct TileSpace {
             }
         } else {
             const uint32_t per_e = (uint32_t)(tiles_m * tiles_n);
-            const int32_t e = (int32_t)(u / per_e);
-            const int32_t rest = (int32_t)(u - (uint32_t)e * per_e);
+            const int32_t e = expert_at(u);
+            const int32_t rest = (int32_t)(u - (u / per_e) * per_e);
             tm = rest / tiles_n;
             tn = rest - tm * tiles_n;
             const int64_t p_e = __builtin_amdgcn_readfirstlane(pad_start[e]);
@@ -749,7 +767,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     constexpr int kStageBytes = kWordsB1 + (B1 ? 1024 : 0);
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];
     __shared__ int32_t pad_start[GMODE == 0 ? 1 : kMaxSegs + 1];
-    __shared__ int32_t tile_start[GMODE == 1 ? kMaxSegs + 1 : 1];
+    __shared__ int32_t tile_start[GMODE != 0 ? kMaxSegs + 1 : 1];     // ragged K: the expert cost order
     __shared__ int32_t seg_start[GMODE == 0 ? 1 : kMaxSegs + 1];     // sanitized segment offsets
     __shared__ __attribute__((aligned(16))) uint8_t qstrip[QOUT ? 4 * kQStrip : 16];
     __shared__ __attribute__((aligned(16))) uint8_t ptab[QSR ? 4 * kPTab : 16];
@@ -765,6 +783,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
                 wave_prefix(gr.nseg, [&](int i) { return (off[i + 1] - off[i] + BM2 - 1) / BM2; }, tile_start);
         }
         __syncthreads();
+        if (GMODE == 2) {
+            // experts by descending K-tile count, ties by index: rank -> expert
+            for (int e = threadIdx.x; e < gr.nseg; e += blockDim.x) {
+                const int32_t ne = pad_start[e + 1] - pad_start[e];
+                int rank = 0;
+                for (int f = 0; f < gr.nseg; ++f) {
+                    const int32_t nf = pad_start[f + 1] - pad_start[f];
+                    rank += (nf > ne || (nf == ne && f < e)) ? 1 : 0;
+                }
+                tile_start[rank] = e;
+            }
+            __syncthreads();
+        }
         if (GMODE == 1) total = (uint32_t)__builtin_amdgcn_readfirstlane(tile_start[gr.nseg]) * (uint32_t)tiles_n;
         else total = (uint32_t)(gr.nseg * tiles_m * tiles_n);
     }
@@ -865,7 +896,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     enter();
     auto advance = [&]() __attribute__((always_inline)) {
         if (++lk < lt.nk) return;
-        const uint32_t v = ts.valid_from(lu + gridDim.x);
+        const uint32_t v = ts.valid_from(ts.step(lu));
         if (v < total) { lu = v; lt = ts.ref(v); lk = 0; enter(); }
         else lk = lt.nk - 1;
     };
@@ -989,7 +1020,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
         // ---- the tile is complete: write it and go on with the next one, whose
         // first K-tiles are already in the ring and first fragments in registers
         store(ct);
-        cu = ts.valid_from(cu + gridDim.x);
+        cu = ts.valid_from(ts.step(cu));
         if (cu >= total) break;
         ct = ts.ref(cu);
 #pragma unroll
