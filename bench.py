@@ -503,6 +503,7 @@ for c in FETCH_SIZE WRITE_SIZE; do
 done
 rocprofv3 --pmc MfmaUtil LdsUtil LDSBankConflict LdsBankConflict --output-format csv -d $O/dense_7b_util -o dense_7b -- python3 $R/bench.py --workload dense_7b --also none --steps 1 --warmup 0 --no-cpu-baseline > $O/dense_7b_util.log 2>&1
 rocprofv3 --pmc TCC_HIT_sum TCC_MISS_sum --output-format csv -d $O/dense_7b_l2 -o dense_7b -- python3 $R/bench.py --workload dense_7b --also none --steps 1 --warmup 0 --no-cpu-baseline > $O/dense_7b_l2.log 2>&1
+rocprofv3 --pmc VALUBusy SALUBusy --output-format csv -d $O/dense_7b_valu -o dense_7b -- python3 $R/bench.py --workload dense_7b --also none --steps 1 --warmup 0 --no-cpu-baseline > $O/dense_7b_valu.log 2>&1
 python3 $R/bench.py --summarize-profiles $O"""
 
 
@@ -552,7 +553,8 @@ def _per_dispatch(dirname):
     return out
 
 
-UTIL_COUNTERS = ("MfmaUtil", "LdsUtil", "LDSBankConflict", "LdsBankConflict", "TCC_HIT_sum", "TCC_MISS_sum")
+UTIL_COUNTERS = ("MfmaUtil", "LdsUtil", "LDSBankConflict", "LdsBankConflict", "TCC_HIT_sum", "TCC_MISS_sum",
+                 "VALUBusy", "SALUBusy")
 
 
 def utilisation(d: str) -> dict:
@@ -562,7 +564,7 @@ def utilisation(d: str) -> dict:
     (conflicts per access), each averaged over dispatches weighted by duration, and
     the L2 hit rate TCC_HIT / (TCC_HIT + TCC_MISS)."""
     acc = {}
-    for sub in ("dense_7b_util", "dense_7b_l2"):
+    for sub in ("dense_7b_util", "dense_7b_l2", "dense_7b_valu"):
         path = os.path.join(d, sub)
         if not os.path.isdir(path):
             continue
@@ -582,7 +584,9 @@ def utilisation(d: str) -> dict:
                      else round(mean["LDSBankConflict"], 2),
                      "lds_bank_conflicts_per_access": None if mean["LdsBankConflict"] is None
                      else round(mean["LdsBankConflict"], 4),
-                     "l2_hit_rate": round(hit / (hit + miss), 4) if hit + miss else None}
+                     "l2_hit_rate": round(hit / (hit + miss), 4) if hit + miss else None,
+                     "valu_busy_pct": None if mean["VALUBusy"] is None else round(mean["VALUBusy"], 2),
+                     "salu_busy_pct": None if mean["SALUBusy"] is None else round(mean["SALUBusy"], 2)}
     return out
 
 
@@ -671,17 +675,19 @@ def summarize_profiles(d: str, out_dir: str):
                                                          t["algorithmic_bytes_per_launch"],
                                                          t["traffic_over_algorithmic"]))
             if wl == "dense_7b" and util:
-                out += ["", "## MFMA and LDS utilisation, L2 hit rate (counter runs of this workload)", "",
+                out += ["", "## MFMA, VALU and LDS utilisation, L2 hit rate (counter runs of this workload)", "",
                         "rocprofv3 derived counters per dispatch, averaged weighted by duration: MfmaUtil, "
-                        "LdsUtil, LDSBankConflict (% of GPU time LDS stalls on bank conflicts), "
-                        "LdsBankConflict (conflicts per access); L2 hit rate = TCC_HIT / (TCC_HIT + TCC_MISS).",
-                        "", "| kind | MfmaUtil % | LdsUtil % | LDSBankConflict % | LdsBankConflict / access | "
-                        "L2 hit rate |", "|---|---|---|---|---|---|"]
+                        "VALUBusy and SALUBusy (% of GPU time the vector / scalar ALUs issue), LdsUtil, "
+                        "LDSBankConflict (% of GPU time LDS stalls on bank conflicts), LdsBankConflict "
+                        "(conflicts per access); L2 hit rate = TCC_HIT / (TCC_HIT + TCC_MISS).",
+                        "", "| kind | MfmaUtil % | VALUBusy % | SALUBusy % | LdsUtil % | LDSBankConflict % | "
+                        "LdsBankConflict / access | L2 hit rate |", "|---|---|---|---|---|---|---|---|"]
                 for kind in kinds:
                     u = util.get(kind)
                     if u:
-                        out.append("| %s | %s | %s | %s | %s | %s |" % (
-                            kind, u["mfma_util_pct"], u["lds_util_pct"], u["lds_bank_conflict_pct_time"],
+                        out.append("| %s | %s | %s | %s | %s | %s | %s | %s |" % (
+                            kind, u["mfma_util_pct"], u.get("valu_busy_pct"), u.get("salu_busy_pct"),
+                            u["lds_util_pct"], u["lds_bank_conflict_pct_time"],
                             u["lds_bank_conflicts_per_access"], u["l2_hit_rate"]))
             out += ["", "## rocprofv3 --stats rows of these kernels (whole benchmark run, all workloads)", "",
                     "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
