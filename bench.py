@@ -100,6 +100,8 @@ def parse():
                                      "dense_7b_yq_separate",
                    help="further workloads measured in the same run (comma list, or 'none')")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--eager", action="store_true",
+                   help="time the steps as eager launches instead of replays of one captured HIP graph")
     p.add_argument("--cpu-sample-tokens", type=int, default=256)
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
     p.add_argument("--hot-loop", default="", choices=["", "gemm", "gemm_fp8", "quant", "quant_sr"],
@@ -394,17 +396,41 @@ class Step:
                 call()
 
 
-def measure(step, torch, steps: int, warmup: int) -> dict:
-    """Wall time of `steps` whole steps, then the same steps with HIP events around
-    every launch (on torch's current stream, the stream the launches go to)."""
+def capture(step, torch):
+    """The step's launches as one HIP graph (torch's graph capture on a side stream,
+    after a warm-up there); the library allocates nothing and issues no memset, so
+    a replay runs exactly the step's kernels without their host launch costs."""
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step.run(record=False)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step.run(record=False)
+    g.replay()
+    torch.cuda.synchronize()
+    return g
+
+
+def measure(step, torch, steps: int, warmup: int, graph: bool = True) -> dict:
+    """Wall time of `steps` whole steps (replays of the step's HIP graph, or eager
+    launches), then the same steps launched eagerly with HIP events around every
+    launch (on torch's current stream, the stream the launches go to)."""
     for _ in range(warmup):
         step.run(record=False)
     torch.cuda.synchronize()
+    g = capture(step, torch) if graph else None
     t0 = time.perf_counter()
     for _ in range(steps):
-        step.run(record=False)
+        if g is not None:
+            g.replay()
+        else:
+            step.run(record=False)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    del g
     step.events = []
     for _ in range(steps):
         step.run(record=True)
@@ -420,7 +446,9 @@ def measure(step, torch, steps: int, warmup: int) -> dict:
     res = {"ms_per_step": ms_per_step, "value": step.flops / (ms_per_step * 1e-3) / 1e12,
            "quant_gb_per_step": sum(o[3] for o in step.ops if o[0].startswith("quant")) / 1e9,
            "kinds": {}, "per_kernel": {},
-           "launches": len(step.ops) * (warmup + 2 * steps)}      # one dispatch per op
+           # one dispatch per op: warm-up, (graph: side-stream warm-up and one untimed
+           # replay,) timed steps, event-timed steps
+           "launches": len(step.ops) * (warmup + 2 * steps + (2 if graph else 0))}
     for kind, (ms, work, n, abytes) in kinds.items():
         bound, peak, unit = KIND_PEAK[kind]
         scale = 1e12 if unit == "TFLOP/s" else 1e9
@@ -724,7 +752,7 @@ def main():
     torch.cuda.set_device(dev)
     w = synth.WORKLOADS[args.workload](device=dev)
     step = Step(q2d, torch, w)
-    res = measure(step, torch, args.steps, args.warmup)
+    res = measure(step, torch, args.steps, args.warmup, graph=not args.eager)
     print("bench: %s measured" % args.workload, file=sys.stderr, flush=True)
     kinds = res["kinds"]
     gemm_kind = max((k for k in kinds if k.startswith("gemm")), key=lambda k: kinds[k]["ms_per_step"])
@@ -753,7 +781,8 @@ def main():
                    "gemm_tflop_per_step": step.flops / 1e12,
                    "quantizer_gb_per_step": round(res["quant_gb_per_step"], 6),
                    "quantizations_per_step": sum(1 for o in step.ops if o[0].startswith("quant")),
-                   "block": w.block},
+                   "block": w.block,
+                   "timed_as": "eager launches" if args.eager else "replays of one captured HIP graph per step"},
         "roofline": roof,
         "quantizer": quant,
         "kinds": kinds,
@@ -769,7 +798,7 @@ def main():
         for name in others:
             wo = synth.WORKLOADS[name](device=dev)
             so = Step(q2d, torch, wo)
-            ro = measure(so, torch, args.steps, args.warmup)
+            ro = measure(so, torch, args.steps, args.warmup, graph=not args.eager)
             print("bench: %s measured" % name, file=sys.stderr, flush=True)
             attach_traffic(name, ro["kinds"])
             rec["other_workloads"][name] = {
