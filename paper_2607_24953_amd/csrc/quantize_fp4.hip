@@ -575,12 +575,13 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
 // Vector-load stochastic-rounding variants at most 168 VGPRs (three waves per
 // SIMD): they are bound by their Philox arithmetic and need the occupancy to
 // hide its latency (the grouped one would otherwise take 169 and drop to two).
-// Dense vector-load round-to-nearest variants at most 128 (four waves per SIMD,
-// two 8-wave workgroups per CU instead of one): 3-5 % more bandwidth despite a
-// few spilled registers.
+// Vector-load round-to-nearest variants at most 128 (four waves per SIMD, two
+// 8-wave workgroups per CU instead of one): 3-8 % more bandwidth despite a few
+// spilled registers (dense: 4, reloaded at the stores; grouped: 12, reloaded once
+// per tile, with the tile's segment held in scalar registers).
 template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED, int WC, bool ONED>
 __global__ __launch_bounds__(256 * WC)
-__attribute__((amdgpu_waves_per_eu(VEC && SR ? 3 : (VEC && !GROUPED ? 4 : 1)))) void fp4_quantize_kernel(QuantArgs a)
+__attribute__((amdgpu_waves_per_eu(VEC && SR ? 3 : (VEC ? 4 : 1)))) void fp4_quantize_kernel(QuantArgs a)
 {
     static_assert(!(ONED && GROUPED), "grouped tensors use 2D blocks");
     constexpr int kTC = 128 * WC;
@@ -601,9 +602,11 @@ __attribute__((amdgpu_waves_per_eu(VEC && SR ? 3 : (VEC && !GROUPED ? 4 : 1)))) 
         for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
             const int64_t rt = tile / tiles_c, tc = tile - rt * tiles_c;
             const int32_t prow = (int32_t)(rt * kTile);
-            const int e = seg_search(pad_start, a.nseg, prow);
-            const int64_t r_begin = off[e], n_e = (int64_t)off[e + 1] - off[e];
-            const int32_t p_e = pad_start[e];
+            // the tile's segment (wave-uniform: scalar registers for the narrowed arguments)
+            const int e = __builtin_amdgcn_readfirstlane(seg_search(pad_start, a.nseg, prow));
+            const int32_t o_e = __builtin_amdgcn_readfirstlane(off[e]);
+            const int64_t r_begin = o_e, n_e = (int64_t)__builtin_amdgcn_readfirstlane(off[e + 1]) - o_e;
+            const int32_t p_e = __builtin_amdgcn_readfirstlane(pad_start[e]);
             QuantArgs b = a;
             b.x = reinterpret_cast<const uint8_t *>(a.x) + r_begin * a.stride_r * (int64_t)sizeof(T);
             b.index_base += r_begin * a.stride_r;
