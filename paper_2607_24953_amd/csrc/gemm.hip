@@ -375,7 +375,7 @@ struct TileSpace {
     int32_t tiles_m, tiles_n;
     const int32_t *pad_start, *tile_start, *seg_start;
     uint32_t total;        // tiles (ragged M: row tiles of all experts x column tiles)
-    uint32_t per, rem, span;   // dense: XCD share of the tile order, group span
+    uint32_t per, rem, span;   // dense and ragged M: XCD share of the tile order; dense: group span
 
     // Ragged K: u is a position in the tile order sorted by cost, experts by
     // descending K-tile count (tile_start holds that expert order), each expert's
@@ -425,8 +425,17 @@ struct TileSpace {
             tm = (int32_t)(first + in % gsz);
             tn = (int32_t)(in / gsz);
         } else if (GMODE == 1) {
-            const int32_t rt = (int32_t)(u / (uint32_t)tiles_n);
-            tn = (int32_t)u - rt * tiles_n;
+            // A multiple of 8 column tiles: the row-major order already gives each
+            // XCD (u mod 8) one column band, i.e. one band of each expert's weight.
+            // Otherwise each XCD takes a contiguous range of that order, so an
+            // expert's weight bands are fetched into one L2 rather than all eight.
+            uint32_t tt = u;
+            if (tiles_n % kXcds != 0) {
+                const uint32_t xcd = u % kXcds, local = u / kXcds;
+                tt = xcd * per + (xcd < rem ? xcd : rem) + local;
+            }
+            const int32_t rt = (int32_t)(tt / (uint32_t)tiles_n);
+            tn = (int32_t)tt - rt * tiles_n;
             const int e = __builtin_amdgcn_readfirstlane(seg_search(tile_start, gr.nseg, rt));
             tm = rt - __builtin_amdgcn_readfirstlane(tile_start[e]);
             const int64_t p_e = __builtin_amdgcn_readfirstlane(pad_start[e]);
@@ -800,8 +809,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
         else total = (uint32_t)(gr.nseg * tiles_m * tiles_n);
     }
     const uint32_t nb = (uint32_t)(tiles_m * tiles_n);
+    const uint32_t ordered = GMODE == 1 ? total : nb;      // tiles of the XCD-contiguous order
     const TileSpace<GMODE, BF16OUT> ts{g, gr, tiles_m, tiles_n, pad_start, tile_start, seg_start, total,
-                                       nb / kXcds, nb % kXcds, (uint32_t)(kGroupM * tiles_n)};
+                                       ordered / kXcds, ordered % kXcds, (uint32_t)(kGroupM * tiles_n)};
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
