@@ -250,6 +250,82 @@ def test_grouped_gemm_ragged_k(q2d, counts, Ng, K):
         assert rel_frob(acc[rows], ref + init[rows]) <= TOL, e
 
 
+def expert_slicer(o, off, trans=False):
+    """expert_rows with the grouped operand dequantized once."""
+    P, C = int(o["padded_rows"][-1]), o["cols"]
+    full = (oracle.dequant_fp4(o["codes_t"], o["scales_t"], C, P) if trans
+            else oracle.dequant_fp4(o["codes"], o["scales"], P, C))
+
+    def rows(e):
+        p, n = int(o["padded_rows"][e]), int(off[e + 1] - off[e])
+        return full[:, p:p + n] if trans else full[p:p + n]
+    return rows
+
+
+def skewed_counts(E, total, seed):
+    """Zipf(1.1)-weighted expert sizes with a few empty experts: many tiles per
+    workgroup, experts of very different K-tile counts and equal ones (ties)."""
+    rng = np.random.default_rng(seed)
+    p = 1.0 / np.arange(1, E + 1) ** 1.1
+    cnt = np.floor(total * p / p.sum()).astype(np.int64)
+    cnt = cnt[rng.permutation(E)]
+    cnt[rng.choice(E, E // 16, replace=False)] = 0
+    return [int(c) for c in cnt]
+
+
+def test_grouped_gemm_ragged_k_many_tiles(q2d):
+    """Weight gradients of 200 Zipf-sized experts (400 output tiles for 256
+    workgroups, walked in the cost-sorted serpentine order): every expert
+    against the oracle."""
+    cnt = skewed_counts(200, 24000, 61)
+    E = len(cnt)
+    off = synth.segment_offsets(cnt)
+    S = int(off[-1])
+    Ng, K = 256, 512
+    dY = synth.normal((S, Ng), 1e-3, 62, torch.bfloat16, device=DEV)
+    X = synth.normal((S, K), 1.0, 63, torch.bfloat16, device=DEV)
+    qdY, odY = quant_grouped(q2d, dY, off, "sr", 7, 2)
+    qX, oX = quant_grouped(q2d, X, off, "rtn")
+    dW = torch.full((E * Ng, K), 7.0, device=DEV)
+    q2d.q2d_grouped_gemm(qdY, 1, qX, 1, dev_offsets(off), out=dW)
+    dW = dW.cpu().numpy()
+    dy_e, x_e = expert_slicer(odY, off, True), expert_slicer(oX, off, True)
+    for e in range(E):
+        rows = slice(e * Ng, (e + 1) * Ng)
+        if off[e] == off[e + 1]:
+            assert np.all(dW[rows] == 0), e
+            continue
+        ref = oracle.gemm(dy_e(e), x_e(e))
+        assert rel_frob(dW[rows], ref) <= TOL, e
+
+
+def test_grouped_gemm_ragged_m_many_tiles(q2d):
+    """Forward GEMMs of 200 Zipf-sized experts with 768-wide outputs (3 column
+    tiles: the XCD-contiguous tile order), several tiles per workgroup: every
+    expert against the oracle, float32 and bf16 outputs."""
+    cnt = skewed_counts(200, 24000, 71)
+    E = len(cnt)
+    off = synth.segment_offsets(cnt)
+    S = int(off[-1])
+    N, K = 768, 256
+    X = synth.normal((S, K), 1.0, 72, torch.bfloat16, device=DEV)
+    W = synth.normal((E * N, K), 0.02, 73, torch.bfloat16, device=DEV)
+    qX, oX = quant_grouped(q2d, X, off, "rtn")
+    qW = q2d.q2d_quantize(W, "rtn")
+    oW = oracle.quantize_fp4_2d(W.cpu(), "rtn")
+    Wf = oracle.operand(oW, False)
+    Y = q2d.q2d_grouped_gemm(qX, 0, qW, 0, dev_offsets(off), out_dtype=torch.float32).cpu().numpy()
+    Yb = q2d.q2d_grouped_gemm(qX, 0, qW, 0, dev_offsets(off), out_dtype=torch.bfloat16).cpu()
+    x_e = expert_slicer(oX, off)
+    for e in range(E):
+        a, b = int(off[e]), int(off[e + 1])
+        if a == b:
+            continue
+        ref = oracle.gemm(x_e(e), Wf[e * N:(e + 1) * N])
+        assert rel_frob(Y[a:b], ref) <= TOL, e
+        check_bf16(Yb[a:b], ref)
+
+
 def test_grouped_gemm_bf16_weight_gradient(q2d):
     off = synth.segment_offsets(COUNTS["edges"])
     E, S = len(COUNTS["edges"]), int(off[-1])
