@@ -62,6 +62,8 @@ __device__ __forceinline__ uint4 load_stream16(const void *p)
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+
 template <typename T>
 struct Elem;
 
@@ -308,20 +310,20 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
     const int e = floor_rule ? fp4_floor_exponent(am) : fp4_block_exponent(am);
     const float scale = bits_f((uint32_t)(127 + e) << 23);       // 2^e
     if (floor_rule && finite) {
-        // saturate magnitudes above 6 * 2^e (exact in bf16: 1.5 * 2^(e+2))
+        // saturate magnitudes above 6 * 2^e (exact in bf16: 1.5 * 2^(e+2)): the
+        // magnitude bits take their minimum with the limit's, the sign stays
+        // (bf16: both halves of a word at once, in place)
         const uint32_t lim = ((uint32_t)(e + 129) << 23) | 0x400000u;
+        const u16x2 l16 = {(uint16_t)(lim >> 16), (uint16_t)(lim >> 16)};
 #pragma unroll
         for (int i = 0; i < 8; ++i)
 #pragma unroll
             for (int k = 0; k < NV; ++k) {
                 if (PK) {
-                    const uint32_t l16 = lim >> 16;
-                    uint32_t lo = v[i][k] & 0xFFFFu, hi = v[i][k] >> 16;
-                    if ((lo & 0x7FFFu) > l16) lo = (lo & 0x8000u) | l16;
-                    if ((hi & 0x7FFFu) > l16) hi = (hi & 0x8000u) | l16;
-                    v[i][k] = lo | (hi << 16);
-                } else if ((v[i][k] & 0x7FFFFFFFu) > lim) {
-                    v[i][k] = (v[i][k] & 0x80000000u) | lim;
+                    const u16x2 mag = __builtin_bit_cast(u16x2, v[i][k] & 0x7FFF7FFFu);
+                    v[i][k] = (v[i][k] & 0x80008000u) | __builtin_bit_cast(uint32_t, __builtin_elementwise_min(mag, l16));
+                } else {
+                    v[i][k] = (v[i][k] & 0x80000000u) | min(v[i][k] & 0x7FFFFFFFu, lim);
                 }
             }
     }
@@ -353,8 +355,13 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
             }
             rowp[i] = w;
         }
+        // 2D blocks: one scale for both layouts, so the column-packed words are
+        // the nibble transpose of the row-packed ones (each element converted
+        // once, and the inputs are dead after the row pass); 1D: every column
+        // has its own scale and is converted on its own
+        if constexpr (!ONED) nibble_transpose8(rowp, colp);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < (ONED ? 8 : 0); ++j) {
             uint32_t w = 0;
             const float sc = cscale(j);
             if (PK) {
@@ -572,13 +579,13 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
     }
 }
 
-// Vector-load stochastic-rounding variants at most 168 VGPRs (three waves per
-// SIMD): they are bound by their Philox arithmetic and need the occupancy to
-// hide its latency (the grouped one would otherwise take 169 and drop to two).
-// Vector-load round-to-nearest variants at most 128 (four waves per SIMD, two
-// 8-wave workgroups per CU instead of one): 3-8 % more bandwidth despite a few
-// spilled registers (dense: 4, reloaded at the stores; grouped: 12, reloaded once
-// per tile, with the tile's segment held in scalar registers).
+// A lane holds its 8 x 8 sub-block (32 registers of bf16 pairs, 64 of float32)
+// and converts each element once, so the bf16 vector-load variants take 91-115
+// VGPRs with nothing spilled (four or five waves per SIMD).  The bounds below
+// (at most 168 VGPRs for stochastic rounding, whose Philox latency needs three
+// waves per SIMD; at most 128 for round to nearest) bind only the float32 ones.
+// Spilled registers cost HBM writes here, not only latency: every wave's spill
+// lines end up evicted by the streaming traffic.
 template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED, int WC, bool ONED>
 __global__ __launch_bounds__(256 * WC)
 __attribute__((amdgpu_waves_per_eu(VEC && SR ? 3 : (VEC ? 4 : 1)))) void fp4_quantize_kernel(QuantArgs a)
@@ -630,10 +637,9 @@ __attribute__((amdgpu_waves_per_eu(VEC && SR ? 3 : (VEC ? 4 : 1)))) void fp4_qua
 template <typename T, bool VEC, bool SR, bool A8, bool G, bool ONED>
 hipError_t launch_t(const QuantArgs &a, hipStream_t s)
 {
-    // round to nearest is bound by memory traffic: 256-column tiles write whole
-    // 128-byte lines of codes.  Stochastic rounding is bound by its Philox work
-    // and keeps 4-wave workgroups for occupancy.
-    constexpr int WC = SR ? 1 : 2;
+    // 256-column tiles of 8 waves in both rounding modes: the row-packed codes
+    // leave as whole 128-byte lines
+    constexpr int WC = 2;
     int64_t nb = (a.rows_pad / kTile) * ((a.cols_pad + 128 * WC - 1) / (128 * WC));
     // grouped: each workgroup walks several tiles, so that the segment table is
     // built once per few tiles (the bound covers every padded segment's tiles);
