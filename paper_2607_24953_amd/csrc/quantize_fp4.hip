@@ -581,9 +581,10 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
 
 // A lane holds its 8 x 8 sub-block (32 registers of bf16 pairs, 64 of float32)
 // and converts each element once, so the bf16 vector-load variants take 91-115
-// VGPRs with nothing spilled (four or five waves per SIMD).  The bounds below
+// VGPRs with nothing spilled (four or five waves per SIMD).  Of the bounds below
 // (at most 168 VGPRs for stochastic rounding, whose Philox latency needs three
-// waves per SIMD; at most 128 for round to nearest) bind only the float32 ones.
+// waves per SIMD; at most 128 for round to nearest) only the float32
+// round-to-nearest variants reach theirs.
 // Spilled registers cost HBM writes here, not only latency: every wave's spill
 // lines end up evicted by the streaming traffic.
 template <typename T, bool VEC, bool SR, bool ALIGNED8, bool GROUPED, int WC, bool ONED>
