@@ -513,6 +513,96 @@ __device__ __forceinline__ void store_block(v16f (&acc)[4][4], uint8_t *cbase, u
         }
 }
 
+// Interleaved columns (the ragged-M grouped kernels): MFMA tiles 2p and 2p + 1
+// of a wave take B rows 64 p + 2 l and
+// 64 p + 2 l + 1 in lane l, so a lane holds two neighbouring output columns of
+// every row it has, and 32 lanes write a row's 64 columns (128 bytes of bf16,
+// 256 of float32) with one store instruction.  Whole-line stores: a CU writes
+// about three times faster than with the two-byte, half-line stores of the
+// plain column order.
+//
+// Write a wave's 128 x 128 accumulator block in that layout at cbase (the
+// block's first element); CHECK masks rows >= rows_left and columns >=
+// cols_left.  PAIR: C allows the 4-byte (bf16) or 8-byte (float32) pair
+// stores (aligned start and row pitch); otherwise each element is stored on
+// its own.  Non-temporal stores, as in store_tile.
+template <bool BF16OUT, bool ACC, bool CHECK, bool PAIR>
+__device__ __forceinline__ void store_block_pairs(v16f (&acc)[4][4], uint8_t *cbase, uint32_t ldc_bytes,
+                                                  int rows_left, int cols_left)
+{
+    typedef __bf16 bf2_t __attribute__((ext_vector_type(2)));
+    typedef float f2_t __attribute__((ext_vector_type(2)));
+    const int lane = threadIdx.x & 63;
+    const int col = 2 * (lane & 31), r4 = 4 * (lane >> 5);
+    const int esize = BF16OUT ? 2 : 4;
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+s"(ldc_bytes));   // and the last MFMA results settle
+    uint32_t rb = (uint32_t)r4 * ldc_bytes + (uint32_t)(col * esize);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int roff = i * 32 + 8 * (r >> 2) + r4 + (r & 3);
+            if (r > 0 || i > 0) rb += (uint32_t)((r & 3) ? 1 : 5) * ldc_bytes;   // next row of this lane
+            if (CHECK && roff >= rows_left) continue;
+#pragma unroll
+            for (int jp = 0; jp < 2; ++jp) {
+                const int c = 64 * jp + col;            // columns c, c + 1 of the block
+                if (CHECK && c >= cols_left) continue;
+                float v0, v1;
+                asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v0) : "a"(acc[i][2 * jp][r]));
+                asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v1) : "a"(acc[i][2 * jp + 1][r]));
+                uint8_t *p = cbase + rb + 64 * jp * esize;
+                const bool both = !CHECK || c + 1 < cols_left;
+                if (PAIR && both) {
+                    if (BF16OUT) {
+                        if (ACC) {
+                            const bf2_t o = *reinterpret_cast<const bf2_t *>(p);
+                            v0 += (float)o.x;
+                            v1 += (float)o.y;
+                        }
+                        const bf2_t b = {(__bf16)v0, (__bf16)v1};
+                        __builtin_nontemporal_store(__builtin_bit_cast(uint32_t, b), reinterpret_cast<uint32_t *>(p));
+                    } else {
+                        if (ACC) {
+                            const f2_t o = *reinterpret_cast<const f2_t *>(p);
+                            v0 += o.x;
+                            v1 += o.y;
+                        }
+                        const f2_t f = {v0, v1};
+                        __builtin_nontemporal_store(f, reinterpret_cast<f2_t *>(p));
+                    }
+                } else {
+                    if (BF16OUT) {
+                        __bf16 *q = reinterpret_cast<__bf16 *>(p);
+                        if (ACC) v0 += (float)q[0];
+                        __builtin_nontemporal_store((__bf16)v0, q);
+                        if (both) {
+                            if (ACC) v1 += (float)q[1];
+                            __builtin_nontemporal_store((__bf16)v1, q + 1);
+                        }
+                    } else {
+                        float *q = reinterpret_cast<float *>(p);
+                        if (ACC) v0 += q[0];
+                        __builtin_nontemporal_store(v0, q);
+                        if (both) {
+                            if (ACC) v1 += q[1];
+                            __builtin_nontemporal_store(v1, q + 1);
+                        }
+                    }
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+}
+
+// Row of B (within a 256-row tile) that feeds MFMA row slot t = 128 h + 32 j + l
+// of the interleaved-column layout: 128 h + 64 (j / 2) + 2 l + j % 2.
+__device__ __forceinline__ int interleaved_row(int t)
+{
+    const int j = (t >> 5) & 3, l = t & 31;
+    return (t & ~127) + 64 * (j >> 1) + 2 * l + (j & 1);
+}
+
 // Quantize a wave's 128 x 128 accumulator block into 2D-block FP4 with round to
 // nearest (the quantizer's scale rule and codec, applied to the float32
 // result): each 32 x 32 MFMA tile is exactly one block.
@@ -774,6 +864,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     constexpr int kWordsA1 = 2 * kCodeBytes + 1024;             // after 2 x codes + 1 KB of 2D scale words: per-row A scale words
     constexpr int kWordsB1 = kWordsA1 + (A1 ? 1024 : 0);       // per-row B scale words
     constexpr int kStageBytes = kWordsB1 + (B1 ? 1024 : 0);
+    // interleaved output columns with pair stores for the ragged-M grouped GEMMs
+    // (bf16 outputs of short-K expert tiles, where the epilogue weighs most)
+    constexpr bool PERM = GMODE == 1;
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];
     __shared__ int32_t pad_start[GMODE == 0 ? 1 : kMaxSegs + 1];
     __shared__ int32_t tile_start[GMODE != 0 ? kMaxSegs + 1 : 1];     // ragged K: the expert cost order
@@ -819,6 +912,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     const int half = lane >> 5;
     const int esize = BF16OUT ? 2 : 4;
     const uint32_t ldc_bytes = (uint32_t)(g.ldc * esize);
+    // pair stores need C and its row pitch aligned to two elements
+    const bool pair_ok = ((reinterpret_cast<uintptr_t>(g.c) | (uintptr_t)ldc_bytes) & (uintptr_t)(2 * esize - 1)) == 0;
 
     v16f acc[4][4];
 #pragma unroll
@@ -839,10 +934,20 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
                 store_qblock<true, QSR>(acc, g, strip, tab, r0, c0, t.M - r0, t.N - c0);
         } else {
             uint8_t *cb = t.c + (int64_t)r0 * ldc_bytes + (int64_t)c0 * esize;
-            if (t.m0 + BM2 <= t.M && t.n0 + BN2 <= t.N)
+            const bool full = t.m0 + BM2 <= t.M && t.n0 + BN2 <= t.N;
+            if constexpr (PERM) {
+                if (full) {
+                    if (pair_ok) store_block_pairs<BF16OUT, ACC, false, true>(acc, cb, ldc_bytes, 128, 128);
+                    else store_block_pairs<BF16OUT, ACC, false, false>(acc, cb, ldc_bytes, 128, 128);
+                } else {
+                    if (pair_ok) store_block_pairs<BF16OUT, ACC, true, true>(acc, cb, ldc_bytes, t.M - r0, t.N - c0);
+                    else store_block_pairs<BF16OUT, ACC, true, false>(acc, cb, ldc_bytes, t.M - r0, t.N - c0);
+                }
+            } else if (full) {
                 store_block<BF16OUT, ACC, false>(acc, cb, ldc_bytes, 128, 128);
-            else
+            } else {
                 store_block<BF16OUT, ACC, true>(acc, cb, ldc_bytes, t.M - r0, t.N - c0);
+            }
         }
     };
 
@@ -884,13 +989,14 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
             lsrcA1 = lt.sa + 4 * r;
         }
         if (B1) {
-            int r = lt.n0 + 64 * wave + lane; r = r < lt.N ? r : lt.N - 1;
+            int r = lt.n0 + (PERM ? interleaved_row(64 * wave + lane) : 64 * wave + lane);
+            r = r < lt.N ? r : lt.N - 1;
             lsrcB1 = lt.sb + 4 * r;
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             int ra = lt.m0 + row[j]; ra = ra < lt.M ? ra : lt.M - 1;
-            int rb = lt.n0 + row[j]; rb = rb < lt.N ? rb : lt.N - 1;
+            int rb = lt.n0 + (PERM ? interleaved_row(row[j]) : row[j]); rb = rb < lt.N ? rb : lt.N - 1;
             offA[j] = (uint32_t)ra * (uint32_t)g.lda + c16[j];
             offB[j] = (uint32_t)rb * (uint32_t)g.ldb + c16[j];
         }
@@ -951,12 +1057,20 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     uint4 fa0[4], fb0[4], fa1[4], fb1[4];
     uint32_t scA[4], scB[4], nA[4], nB[4];
 
+    // the B block-row word of MFMA tile j: with interleaved columns, lanes 0..15
+    // (rows 2 l + j % 2 < 32 of the tile pair) take block row 2 (j / 2), lanes
+    // 16..31 the next one; 1D words already belong to the lane's own row
+    auto bword = [&](const uint32_t (&w)[4], int j) __attribute__((always_inline)) -> uint32_t {
+        if (!PERM || B1) return w[j];
+        return (lane & 16) ? w[2 * (j >> 1) + 1] : w[2 * (j >> 1)];
+    };
+
 #define Q2D_MFMA(fa, fb, scA_, scB_, ks, i, j)                                                          \
     do {                                                                                             \
         const v8i av_ = {(int)fa[i].x, (int)fa[i].y, (int)fa[i].z, (int)fa[i].w, 0, 0, 0, 0};       \
         const v8i bv_ = {(int)fb[j].x, (int)fb[j].y, (int)fb[j].z, (int)fb[j].w, 0, 0, 0, 0};       \
         const int sa_ = (int)((scA_[i] >> (8 * (2 * (ks) + half))) & 0xFFu);                         \
-        const int sb_ = (int)((scB_[j] >> (8 * (2 * (ks) + half))) & 0xFFu);                         \
+        const int sb_ = (int)((bword(scB_, j) >> (8 * (2 * (ks) + half))) & 0xFFu);                  \
         acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av_, bv_, acc[i][j], F::kCbsz,   \
                                                                     F::kCbsz, 0, sa_, 0, sb_);       \
     } while (0)
