@@ -513,13 +513,12 @@ __device__ __forceinline__ void store_block(v16f (&acc)[4][4], uint8_t *cbase, u
         }
 }
 
-// Interleaved columns (the ragged-M grouped kernels): MFMA tiles 2p and 2p + 1
-// of a wave take B rows 64 p + 2 l and
-// 64 p + 2 l + 1 in lane l, so a lane holds two neighbouring output columns of
-// every row it has, and 32 lanes write a row's 64 columns (128 bytes of bf16,
-// 256 of float32) with one store instruction.  Whole-line stores: a CU writes
-// about three times faster than with the two-byte, half-line stores of the
-// plain column order.
+// Interleaved columns (the persistent kernels with bf16 output): MFMA tiles 2p
+// and 2p + 1 of a wave take B rows 64 p + 2 l and 64 p + 2 l + 1 in lane l, so
+// a lane holds two neighbouring output columns of every row it has, and 32
+// lanes write a row's 64 columns (128 bytes of bf16) with one store
+// instruction.  Whole-line stores: a CU writes about three times faster than
+// with the two-byte, half-line stores of the plain column order.
 //
 // Write a wave's 128 x 128 accumulator block in that layout at cbase (the
 // block's first element); CHECK masks rows >= rows_left and columns >=
@@ -864,9 +863,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
     constexpr int kWordsA1 = 2 * kCodeBytes + 1024;             // after 2 x codes + 1 KB of 2D scale words: per-row A scale words
     constexpr int kWordsB1 = kWordsA1 + (A1 ? 1024 : 0);       // per-row B scale words
     constexpr int kStageBytes = kWordsB1 + (B1 ? 1024 : 0);
-    // interleaved output columns with pair stores for the ragged-M grouped GEMMs
-    // (bf16 outputs of short-K expert tiles, where the epilogue weighs most)
-    constexpr bool PERM = GMODE == 1;
+    // interleaved output columns with pair stores for bf16 outputs (3-7 % faster
+    // at K <= 4096, where the epilogue weighs most); float32 rows already leave
+    // as whole lines, and pairs of them measured slower
+    constexpr bool PERM = BF16OUT && !QOUT;
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kStages * kStageBytes];
     __shared__ int32_t pad_start[GMODE == 0 ? 1 : kMaxSegs + 1];
     __shared__ int32_t tile_start[GMODE != 0 ? kMaxSegs + 1 : 1];     // ragged K: the expert cost order
