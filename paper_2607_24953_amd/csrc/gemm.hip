@@ -521,21 +521,19 @@ __device__ __forceinline__ void store_block(v16f (&acc)[4][4], uint8_t *cbase, u
 // with the two-byte, half-line stores of the plain column order.
 //
 // Write a wave's 128 x 128 accumulator block in that layout at cbase (the
-// block's first element); CHECK masks rows >= rows_left and columns >=
-// cols_left.  PAIR: C allows the 4-byte (bf16) or 8-byte (float32) pair
-// stores (aligned start and row pitch); otherwise each element is stored on
+// block's first element) as bf16, rounded to nearest even; CHECK masks rows >=
+// rows_left and columns >= cols_left.  PAIR: C allows the 4-byte pair stores
+// (start and row pitch 4-byte aligned); otherwise each element is stored on
 // its own.  Non-temporal stores, as in store_tile.
-template <bool BF16OUT, bool ACC, bool CHECK, bool PAIR>
+template <bool ACC, bool CHECK, bool PAIR>
 __device__ __forceinline__ void store_block_pairs(v16f (&acc)[4][4], uint8_t *cbase, uint32_t ldc_bytes,
                                                   int rows_left, int cols_left)
 {
     typedef __bf16 bf2_t __attribute__((ext_vector_type(2)));
-    typedef float f2_t __attribute__((ext_vector_type(2)));
     const int lane = threadIdx.x & 63;
     const int col = 2 * (lane & 31), r4 = 4 * (lane >> 5);
-    const int esize = BF16OUT ? 2 : 4;
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+s"(ldc_bytes));   // and the last MFMA results settle
-    uint32_t rb = (uint32_t)r4 * ldc_bytes + (uint32_t)(col * esize);
+    uint32_t rb = (uint32_t)r4 * ldc_bytes + (uint32_t)(col * 2);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -550,43 +548,23 @@ __device__ __forceinline__ void store_block_pairs(v16f (&acc)[4][4], uint8_t *cb
                 float v0, v1;
                 asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v0) : "a"(acc[i][2 * jp][r]));
                 asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v1) : "a"(acc[i][2 * jp + 1][r]));
-                uint8_t *p = cbase + rb + 64 * jp * esize;
+                uint8_t *p = cbase + rb + 64 * jp * 2;
                 const bool both = !CHECK || c + 1 < cols_left;
                 if (PAIR && both) {
-                    if (BF16OUT) {
-                        if (ACC) {
-                            const bf2_t o = *reinterpret_cast<const bf2_t *>(p);
-                            v0 += (float)o.x;
-                            v1 += (float)o.y;
-                        }
-                        const bf2_t b = {(__bf16)v0, (__bf16)v1};
-                        __builtin_nontemporal_store(__builtin_bit_cast(uint32_t, b), reinterpret_cast<uint32_t *>(p));
-                    } else {
-                        if (ACC) {
-                            const f2_t o = *reinterpret_cast<const f2_t *>(p);
-                            v0 += o.x;
-                            v1 += o.y;
-                        }
-                        const f2_t f = {v0, v1};
-                        __builtin_nontemporal_store(f, reinterpret_cast<f2_t *>(p));
+                    if (ACC) {
+                        const bf2_t o = *reinterpret_cast<const bf2_t *>(p);
+                        v0 += (float)o.x;
+                        v1 += (float)o.y;
                     }
+                    const bf2_t b = {(__bf16)v0, (__bf16)v1};
+                    __builtin_nontemporal_store(__builtin_bit_cast(uint32_t, b), reinterpret_cast<uint32_t *>(p));
                 } else {
-                    if (BF16OUT) {
-                        __bf16 *q = reinterpret_cast<__bf16 *>(p);
-                        if (ACC) v0 += (float)q[0];
-                        __builtin_nontemporal_store((__bf16)v0, q);
-                        if (both) {
-                            if (ACC) v1 += (float)q[1];
-                            __builtin_nontemporal_store((__bf16)v1, q + 1);
-                        }
-                    } else {
-                        float *q = reinterpret_cast<float *>(p);
-                        if (ACC) v0 += q[0];
-                        __builtin_nontemporal_store(v0, q);
-                        if (both) {
-                            if (ACC) v1 += q[1];
-                            __builtin_nontemporal_store(v1, q + 1);
-                        }
+                    __bf16 *q = reinterpret_cast<__bf16 *>(p);
+                    if (ACC) v0 += (float)q[0];
+                    __builtin_nontemporal_store((__bf16)v0, q);
+                    if (both) {
+                        if (ACC) v1 += (float)q[1];
+                        __builtin_nontemporal_store((__bf16)v1, q + 1);
                     }
                 }
             }
@@ -937,11 +915,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp4_persistent_kernel(GemmAr
             const bool full = t.m0 + BM2 <= t.M && t.n0 + BN2 <= t.N;
             if constexpr (PERM) {
                 if (full) {
-                    if (pair_ok) store_block_pairs<BF16OUT, ACC, false, true>(acc, cb, ldc_bytes, 128, 128);
-                    else store_block_pairs<BF16OUT, ACC, false, false>(acc, cb, ldc_bytes, 128, 128);
+                    if (pair_ok) store_block_pairs<ACC, false, true>(acc, cb, ldc_bytes, 128, 128);
+                    else store_block_pairs<ACC, false, false>(acc, cb, ldc_bytes, 128, 128);
                 } else {
-                    if (pair_ok) store_block_pairs<BF16OUT, ACC, true, true>(acc, cb, ldc_bytes, t.M - r0, t.N - c0);
-                    else store_block_pairs<BF16OUT, ACC, true, false>(acc, cb, ldc_bytes, t.M - r0, t.N - c0);
+                    if (pair_ok) store_block_pairs<ACC, true, true>(acc, cb, ldc_bytes, t.M - r0, t.N - c0);
+                    else store_block_pairs<ACC, true, false>(acc, cb, ldc_bytes, t.M - r0, t.N - c0);
                 }
             } else if (full) {
                 store_block<BF16OUT, ACC, false>(acc, cb, ldc_bytes, 128, 128);
