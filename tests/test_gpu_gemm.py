@@ -97,6 +97,31 @@ def test_gemm_fp4_multi_tile_per_workgroup(q2d, M, N, K, ta, tb):
     check_bf16(c16, ref + c0.float().cpu().numpy().astype(np.float64))
 
 
+# bf16 output of the persistent kernel into views of a wider buffer: an even
+# row pitch (whole-line pair stores), an odd one and a base one element off
+# (both one store per element), with and without accumulation; N is odd, so the
+# last column of every row is a lone element.  Nothing outside the view changes.
+@pytest.mark.parametrize("pad,base", [(6, 0), (1, 0), (2, 1)])
+@pytest.mark.parametrize("acc", [False, True])
+def test_gemm_bf16_strided_output(q2d, pad, base, acc):
+    M, N, K = 2100, 4001, 384                       # 9 x 16 output tiles of 256 x 256
+    A = synth.normal((M, K), 1.0, 31, torch.bfloat16, device=DEV)
+    B = synth.normal((N, K), 0.02, 32, torch.bfloat16, device=DEV)
+    qa, oa = quant(q2d, A, "rtn")
+    qb, ob = quant(q2d, B, "sr", 5, 1)
+    ref = oracle.gemm(oracle.operand(oa, False), oracle.operand(ob, False))
+    ld = N + pad
+    flat = synth.normal((M * ld + 2,), 0.5, 33, torch.bfloat16, device=DEV)
+    before = flat.clone()
+    c = flat[base:base + M * ld].view(M, ld)[:, :N]
+    c0 = c.float().cpu().numpy().astype(np.float64)
+    q2d.q2d_gemm(qa, 0, qb, 0, out=c, accumulate=acc)
+    check_bf16(c, ref + c0 if acc else ref)
+    inside = torch.zeros(M * ld + 2, dtype=torch.bool, device=DEV)
+    inside[base:base + M * ld].view(M, ld)[:, :N] = True
+    assert torch.equal(flat.view(torch.int16)[~inside], before.view(torch.int16)[~inside])
+
+
 def test_gemm_deterministic(q2d):
     """Two runs of each persistent-kernel GEMM (forward with bf16 output, weight
     gradient with fp32 output, the quantizing epilogue) on the same operands give
