@@ -1180,6 +1180,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
     const int half = lane >> 5;
     const uint32_t nk = (uint32_t)(g.K / 64);       // K is a multiple of 128
     const uint32_t nw = (uint32_t)(g.K / 128);      // scale words per row (S16: at least 4)
+    // bf16 output: interleaved output columns with pair stores, as in the FP4
+    // kernel (the per-row scale words follow their rows)
+    constexpr bool PERM = BF16OUT;
 
     // codes: DMA j of this wave fills bytes [(4j + wave) * 1024, +1024) of an
     // operand stage (rows 16 (4j + wave) + lane / 4, physical chunk lane % 4,
@@ -1191,14 +1194,15 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
         const int row = 16 * (4 * j + wave) + (lane >> 2);
         const int c = (lane & 3) ^ Fmt<kFmtFp4Block2D>::swz(row);
         int64_t ra = m0 + row; ra = ra < g.M ? ra : g.M - 1;
-        int64_t rb = n0 + row; rb = rb < g.N ? rb : g.N - 1;
+        int64_t rb = n0 + (PERM ? interleaved_row(row) : row); rb = rb < g.N ? rb : g.N - 1;
         offA[j] = (uint32_t)(ra * g.lda + c * 16);
         offB[j] = (uint32_t)(rb * g.ldb + c * 16);
     }
     uint32_t soffA, soffB;
     {
         int64_t ra = m0 + 64 * wave + lane; ra = ra < g.M ? ra : g.M - 1;
-        int64_t rb = n0 + 64 * wave + lane; rb = rb < g.N ? rb : g.N - 1;
+        int64_t rb = n0 + (PERM ? interleaved_row(64 * wave + lane) : 64 * wave + lane);
+        rb = rb < g.N ? rb : g.N - 1;
         soffA = (uint32_t)(ra * g.ldsa);
         soffB = (uint32_t)(rb * g.ldsb);
     }
@@ -1368,12 +1372,25 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_fp8_256_kernel(GemmArgs g, i
     }
 #undef Q2D_RD8
 
-    const int64_t row0 = m0 + wm * 128 + 4 * half;
-    const int64_t col0 = n0 + wn * 128 + (lane & 31);
-    if (m0 + BM2 <= g.M && n0 + BN2 <= g.N) {
-        store_tile<BF16OUT, ACC, false>(acc, g, row0, col0);
+    const bool full = m0 + BM2 <= g.M && n0 + BN2 <= g.N;
+    if constexpr (PERM) {
+        const uint32_t ldc_bytes = (uint32_t)(g.ldc * 2);
+        const bool pair_ok = ((reinterpret_cast<uintptr_t>(g.c) | (uintptr_t)ldc_bytes) & 3u) == 0;
+        const int64_t r0 = m0 + wm * 128, cl0 = n0 + wn * 128;
+        uint8_t *cb = reinterpret_cast<uint8_t *>(g.c) + r0 * ldc_bytes + cl0 * 2;
+        const int rows_left = (int)(g.M - r0), cols_left = (int)(g.N - cl0);
+        if (full) {
+            if (pair_ok) store_block_pairs<ACC, false, true>(acc, cb, ldc_bytes, 128, 128);
+            else store_block_pairs<ACC, false, false>(acc, cb, ldc_bytes, 128, 128);
+        } else {
+            if (pair_ok) store_block_pairs<ACC, true, true>(acc, cb, ldc_bytes, rows_left, cols_left);
+            else store_block_pairs<ACC, true, false>(acc, cb, ldc_bytes, rows_left, cols_left);
+        }
     } else {
-        store_tile<BF16OUT, ACC, true>(acc, g, row0, col0);
+        const int64_t row0 = m0 + wm * 128 + 4 * half;
+        const int64_t col0 = n0 + wn * 128 + (lane & 31);
+        if (full) store_tile<BF16OUT, ACC, false>(acc, g, row0, col0);
+        else store_tile<BF16OUT, ACC, true>(acc, g, row0, col0);
     }
 }
 
