@@ -46,7 +46,10 @@ namespace {
 
 constexpr int BM = 128, BN = 128, BK = 128;
 constexpr int kThreads = 256;
-constexpr int kGroupM = 8;
+// row tiles per group of the XCD-aware raster: an XCD's 32 concurrent tiles
+// form a 4 x 8 block, whose four A row panels (512 KB each at K = 4096) stay
+// resident in its 4 MB L2 while the B panels stream past
+constexpr int kGroupM = 4;
 constexpr int kXcds = 8;
 
 template <int FMT>
