@@ -227,10 +227,16 @@ def kind_of(kernel_name: str):
 
 
 def source_hash(*names) -> str:
+    """Hash of the code of the named kernel sources: comments and whitespace are
+    dropped first, so that an edit of a comment does not count as a change of
+    the kernel the counters were taken on."""
+    import re
     h = hashlib.sha256()
     for n in names:
-        with open(os.path.join(HERE, "paper_2607_24953_amd", "csrc", n), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(HERE, "paper_2607_24953_amd", "csrc", n), encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"//[^\n]*|/\*.*?\*/", "", text, flags=re.S)
+        h.update(re.sub(r"\s+", "", text).encode())
     return h.hexdigest()[:16]
 
 
