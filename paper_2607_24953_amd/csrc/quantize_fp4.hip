@@ -355,33 +355,36 @@ __device__ __forceinline__ void quantize_tile(QuantArgs a, const int64_t tr, con
             }
             rowp[i] = w;
         }
-        // 2D blocks: one scale for both layouts, so the column-packed words are
-        // the nibble transpose of the row-packed ones (each element converted
-        // once, and the inputs are dead after the row pass); 1D: every column
-        // has its own scale and is converted on its own
-        if constexpr (!ONED) nibble_transpose8(rowp, colp);
+        if constexpr (!ONED) {
+            // 2D blocks: one scale for both layouts, so the column-packed words are
+            // the nibble transpose of the row-packed ones (each element converted
+            // once, and the inputs are dead after the row pass)
+            nibble_transpose8(rowp, colp);
+        } else {
+            // 1D: every column has its own scale and is converted on its own
 #pragma unroll
-        for (int j = 0; j < (ONED ? 8 : 0); ++j) {
-            uint32_t w = 0;
-            const float sc = cscale(j);
-            if (PK) {
-                // rows (2m, 2m+1) of column j as one packed pair
-                const int k = j >> 1;
-                auto pr = [&](int m) -> uint32_t {
-                    const uint32_t lo = v[2 * m][k], hi = v[2 * m + 1][k];
-                    return (j & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-                };
-                w = rtn_pair_bf16<0>(w, pr(0), sc);
-                w = rtn_pair_bf16<1>(w, pr(1), sc);
-                w = rtn_pair_bf16<2>(w, pr(2), sc);
-                w = rtn_pair_bf16<3>(w, pr(3), sc);
-            } else {
-                w = rtn_pair_f32<0>(w, elem(0, j), elem(1, j), sc);
-                w = rtn_pair_f32<1>(w, elem(2, j), elem(3, j), sc);
-                w = rtn_pair_f32<2>(w, elem(4, j), elem(5, j), sc);
-                w = rtn_pair_f32<3>(w, elem(6, j), elem(7, j), sc);
+            for (int j = 0; j < 8; ++j) {
+                uint32_t w = 0;
+                const float sc = cscale(j);
+                if (PK) {
+                    // rows (2m, 2m+1) of column j as one packed pair
+                    const int k = j >> 1;
+                    auto pr = [&](int m) -> uint32_t {
+                        const uint32_t lo = v[2 * m][k], hi = v[2 * m + 1][k];
+                        return (j & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
+                    };
+                    w = rtn_pair_bf16<0>(w, pr(0), sc);
+                    w = rtn_pair_bf16<1>(w, pr(1), sc);
+                    w = rtn_pair_bf16<2>(w, pr(2), sc);
+                    w = rtn_pair_bf16<3>(w, pr(3), sc);
+                } else {
+                    w = rtn_pair_f32<0>(w, elem(0, j), elem(1, j), sc);
+                    w = rtn_pair_f32<1>(w, elem(2, j), elem(3, j), sc);
+                    w = rtn_pair_f32<2>(w, elem(4, j), elem(5, j), sc);
+                    w = rtn_pair_f32<3>(w, elem(6, j), elem(7, j), sc);
+                }
+                colp[j] = w;
             }
-            colp[j] = w;
         }
     } else {
         const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
