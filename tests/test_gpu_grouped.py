@@ -326,6 +326,37 @@ def test_grouped_gemm_ragged_m_many_tiles(q2d):
         check_bf16(Yb[a:b], ref)
 
 
+@pytest.mark.parametrize("pad,base", [(1, 0), (2, 1)])
+def test_grouped_gemm_ragged_m_bf16_strided_output(q2d, pad, base):
+    """bf16 ragged-M output into a view of a wider buffer with an odd row pitch or a
+    base one element off (one store per element instead of pair stores): every
+    expert against the oracle, the bytes outside the view unchanged."""
+    cnt = skewed_counts(64, 12000, 81)
+    E = len(cnt)
+    off = synth.segment_offsets(cnt)
+    S = int(off[-1])
+    N, K = 768, 256
+    X = synth.normal((S, K), 1.0, 82, torch.bfloat16, device=DEV)
+    W = synth.normal((E * N, K), 0.02, 83, torch.bfloat16, device=DEV)
+    qX, oX = quant_grouped(q2d, X, off, "rtn")
+    qW = q2d.q2d_quantize(W, "rtn")
+    Wf = oracle.operand(oracle.quantize_fp4_2d(W.cpu(), "rtn"), False)
+    ld = N + pad
+    flat = synth.normal((S * ld + 2,), 0.5, 84, torch.bfloat16, device=DEV)
+    before = flat.clone()
+    y = flat[base:base + S * ld].view(S, ld)[:, :N]
+    q2d.q2d_grouped_gemm(qX, 0, qW, 0, dev_offsets(off), out=y)
+    Yb = y.cpu()
+    x_e = expert_slicer(oX, off)
+    for e in range(E):
+        a, b = int(off[e]), int(off[e + 1])
+        if a < b:
+            check_bf16(Yb[a:b], oracle.gemm(x_e(e), Wf[e * N:(e + 1) * N]))
+    inside = torch.zeros(S * ld + 2, dtype=torch.bool, device=DEV)
+    inside[base:base + S * ld].view(S, ld)[:, :N] = True
+    assert torch.equal(flat.view(torch.int16)[~inside], before.view(torch.int16)[~inside])
+
+
 def test_grouped_gemm_bf16_weight_gradient(q2d):
     off = synth.segment_offsets(COUNTS["edges"])
     E, S = len(COUNTS["edges"]), int(off[-1])
