@@ -122,6 +122,32 @@ def test_gemm_bf16_strided_output(q2d, pad, base, acc):
     assert torch.equal(flat.view(torch.int16)[~inside], before.view(torch.int16)[~inside])
 
 
+@pytest.mark.parametrize("pad,base", [(1, 0), (2, 1)])
+def test_gemm_mxfp8_bf16_strided_output(q2d, pad, base):
+    """The large-tile MXFP8 kernel's bf16 output into a view of a wider buffer with
+    an odd row pitch or a base one element off (one store per element) equals,
+    byte for byte, the same GEMM written contiguously (pair stores), with and
+    without accumulation; the bytes outside the view are unchanged."""
+    M, N, K = 2100, 4001, 512                       # 9 x 16 output tiles of 256 x 256
+    A = synth.normal((M, K), 1.0, 41, torch.bfloat16, device=DEV)
+    B = synth.normal((N, K), 0.02, 42, torch.bfloat16, device=DEV)
+    qa, qb = q2d.mxfp8_quantize(A), q2d.mxfp8_quantize(B)
+    ld = N + pad
+    flat = synth.normal((M * ld + 2,), 0.5, 43, torch.bfloat16, device=DEV)
+    before = flat.clone()
+    c = flat[base:base + M * ld].view(M, ld)[:, :N]
+    ref = c.contiguous()
+    q2d.q2d_gemm(qa, 0, qb, 0, out=c, accumulate=True)
+    q2d.q2d_gemm(qa, 0, qb, 0, out=ref, accumulate=True)
+    assert torch.equal(c.contiguous().view(torch.int16), ref.view(torch.int16))
+    inside = torch.zeros(M * ld + 2, dtype=torch.bool, device=DEV)
+    inside[base:base + M * ld].view(M, ld)[:, :N] = True
+    assert torch.equal(flat.view(torch.int16)[~inside], before.view(torch.int16)[~inside])
+    q2d.q2d_gemm(qa, 0, qb, 0, out=c)
+    q2d.q2d_gemm(qa, 0, qb, 0, out=ref)
+    assert torch.equal(c.contiguous().view(torch.int16), ref.view(torch.int16))
+
+
 def test_gemm_deterministic(q2d):
     """Two runs of each persistent-kernel GEMM (forward with bf16 output, weight
     gradient with fp32 output, the quantizing epilogue) on the same operands give
