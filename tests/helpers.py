@@ -51,3 +51,13 @@ def grouped_written(q, P: int) -> dict:
     return {"codes": q.codes[:P].cpu().numpy(), "scales": q.scales[:P // 32].cpu().numpy(),
             "codes_t": q.codes_t[:, :P // 2].cpu().numpy(),
             "scales_t": q.scales_t[:, :P // 32].cpu().numpy()}
+
+
+def check_bf16(got, ref):
+    """bf16 output = RNE(fp32 accumulation): within 2^-9 |ref| of the fp32 value, which is
+    itself within the fp32 accumulation error (taken as 1e-5 * rms(ref)) of the exact result."""
+    got = got.float().cpu().numpy().astype(np.float64)
+    err = np.abs(got - ref)
+    rms = float(np.sqrt(np.mean(ref * ref))) if ref.size else 0.0
+    tol = np.abs(ref) * 2.0 ** -8 + 1e-5 * rms + 1e-38
+    assert np.all(err <= tol), float((err / tol).max())

@@ -15,7 +15,7 @@ import torch
 import fp8_mfma_model as fm
 import oracle
 import synth
-from helpers import as_oracle_tensor, assert_same_bytes, gpu_buffers, rel_frob
+from helpers import as_oracle_tensor, assert_same_bytes, check_bf16, gpu_buffers, rel_frob
 
 pytestmark = pytest.mark.gpu
 
@@ -36,16 +36,6 @@ def quant(q2d, x, mode, seed=0, offset=0):
     o = oracle.quantize_fp4_2d(x.cpu(), mode, seed, offset)
     assert_same_bytes(gpu_buffers(q), o, "operand")
     return q, o
-
-
-def check_bf16(got, ref):
-    """bf16 output = RNE(fp32 accumulation): within 2^-9 |ref| of the fp32 value, which is
-    itself within the fp32 accumulation error (taken as 1e-5 * rms(ref)) of the exact result."""
-    got = got.float().cpu().numpy().astype(np.float64)
-    err = np.abs(got - ref)
-    rms = float(np.sqrt(np.mean(ref * ref))) if ref.size else 0.0
-    tol = np.abs(ref) * 2.0 ** -8 + 1e-5 * rms + 1e-38
-    assert np.all(err <= tol), float((err / tol).max())
 
 
 GEMM_SHAPES = [(128, 256, 256), (300, 200, 160), (257, 129, 96), (1, 1, 32), (64, 640, 1000),

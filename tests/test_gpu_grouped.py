@@ -21,7 +21,7 @@ import torch
 
 import oracle
 import synth
-from helpers import assert_same_bytes, gpu_buffers, rel_frob
+from helpers import assert_same_bytes, check_bf16, gpu_buffers, rel_frob
 
 pytestmark = pytest.mark.gpu
 
@@ -102,6 +102,65 @@ def test_grouped_equals_per_expert_calls(q2d, counts, C):
                 assert torch.equal(got[k], want[k]), (counts, C, e, n, k)
             P += np_
 
+
+
+@pytest.mark.parametrize("counts", list(COUNTS))
+@pytest.mark.parametrize("C", [96, 200, 384])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("mode", ["rtn", "sr"])
+def test_grouped_quantize(q2d, counts, C, dtype, mode):
+    off = synth.segment_offsets(COUNTS[counts])
+    S = int(off[-1])
+    x = synth.normal((S, C), 1.0, S + C, dtype, device=DEV)
+    synth.add_outlier_channels(x, 3, frac=0.05)
+    q = q2d.q2d_grouped_quantize(x, dev_offsets(off), mode, 5, 11)
+    q.codes.fill_(0xAA), q.codes_t.fill_(0xAA), q.scales.fill_(0xAA), q.scales_t.fill_(0xAA)
+    q2d.q2d_grouped_quantize(x, dev_offsets(off), mode, 5, 11, out=q)
+    o = oracle.quantize_fp4_grouped(x.cpu(), off, mode, 5, 11)
+    assert_grouped_equal(q, o, "%s C=%d %s %s" % (counts, C, dtype, mode))
+
+
+@pytest.mark.parametrize("mode", ["rtn", "sr"])
+@pytest.mark.parametrize("dtype,stride", [(torch.bfloat16, 264), (torch.bfloat16, 261),
+                                          (torch.float32, 260)])
+def test_grouped_quantize_row_stride(q2d, mode, dtype, stride):
+    """Rows of x taken from a wider buffer (row stride > cols): vector loads with
+    8-aligned storage indices (264), element-wise loads (261), and vector loads
+    whose rows start off the 8-element Philox block (fp32, 260)."""
+    off = synth.segment_offsets(COUNTS["edges"])
+    S = int(off[-1])
+    base = synth.normal((S, stride), 1.0, 77, dtype, device=DEV)
+    x = base[:, :200]
+    x_cpu = base.cpu()[:, :200]
+    quant_grouped(q2d, x, off, mode, 3, 0, x_cpu=x_cpu)
+
+
+def test_grouped_quantize_max_experts(q2d):
+    """1024 experts (the maximum), mostly tiny segments; 1025 is rejected."""
+    rng = np.random.default_rng(8)
+    counts = rng.integers(0, 40, 1024)
+    counts[::97] = 129
+    off = synth.segment_offsets(counts)
+    S = int(off[-1])
+    x = synth.normal((S, 128), 1.0, 9, torch.bfloat16, device=DEV)
+    quant_grouped(q2d, x, off, "sr", 1, 2)
+    bad = synth.segment_offsets(np.ones(1025, dtype=np.int64))
+    xb = synth.normal((1025, 64), 1.0, 9, torch.bfloat16, device=DEV)
+    with pytest.raises(q2d.Q2DError):
+        q2d.q2d_grouped_quantize(xb, dev_offsets(bad), "rtn")
+
+
+# ------------------------------------------------------------------ GEMMs
+
+def expert_rows(o, off, e, trans=False):
+    """float64 operand rows of expert e from an oracle grouped quantization:
+    the row-packed copy [n_e, C] or (trans) the column-packed copy [C, n_e]."""
+    P = int(o["padded_rows"][-1])
+    p, n = int(o["padded_rows"][e]), int(off[e + 1] - off[e])
+    C = o["cols"]
+    if not trans:
+        return oracle.dequant_fp4(o["codes"], o["scales"], P, C)[p:p + n]
+    return oracle.dequant_fp4(o["codes_t"], o["scales_t"], C, P)[:, p:p + n]
 
 
 @pytest.mark.parametrize("counts", list(COUNTS))

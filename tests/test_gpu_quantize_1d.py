@@ -18,7 +18,7 @@ import torch
 
 import oracle
 import synth
-from helpers import assert_same_bytes, gpu_buffers, poison, rel_frob
+from helpers import assert_same_bytes, check_bf16, gpu_buffers, poison, rel_frob
 
 pytestmark = pytest.mark.gpu
 
@@ -170,6 +170,9 @@ def test_gemm_with_1d_operands(q2d, M, N, K, ta, tb, fa, fb):
     ref = oracle.gemm(oracle.operand(oa, bool(ta), fa), oracle.operand(ob, bool(tb), fb))
     c32 = q2d.q2d_gemm(qa, ta, qb, tb, out_dtype=torch.float32)
     assert rel_frob(c32.cpu().numpy(), ref) <= TOL
+    # bf16 output: on the persistent kernel, interleaved output columns (a 1D B
+    # operand's row words follow its permuted rows)
+    check_bf16(q2d.q2d_gemm(qa, ta, qb, tb, out_dtype=torch.bfloat16), ref)
 
 
 @pytest.mark.parametrize("T,N,K", [(256, 384, 512), (4096, 2048, 1024)])
