@@ -773,33 +773,19 @@ __device__ __forceinline__ void store_qblock(v16f (&acc)[4][4], const GemmArgs &
             const uint2 run = make_uint2((first & 0xFFFFu) | (second << 16), (first >> 16) | (second & 0xFFFF0000u));
             if (tc + col < g.N && tr < padm)
                 *reinterpret_cast<uint2 *>(g.qct + (int64_t)(tc + col) * g.ldqct + tr / 2 + 8 * h) = run;
-            // row-packed: the neighbouring column's values through a quad permute
-            uint32_t rowb[2] = {0, 0};
-#pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const float send = odd ? v[k] : v[8 + k];      // what the neighbour packs
-                const float nb = __int_as_float(__builtin_amdgcn_update_dpp(
-                    __float_as_int(send), __float_as_int(send), 0xB1, 0xF, 0xF, false));
-                const float own = odd ? v[8 + k] : v[k];
-                const float lo = odd ? nb : own, hi = odd ? own : nb;
-                uint32_t &w = rowb[k >> 2];
-                if constexpr (SR) {
-                    // the neighbour's draw travels with its value
-                    const uint32_t r_lo = rr(k), r_hi = rr(8 + k);
-                    const uint32_t sendr = odd ? r_lo : r_hi;
-                    const uint32_t nbr = (uint32_t)__builtin_amdgcn_update_dpp((int)sendr, (int)sendr, 0xB1, 0xF, 0xF,
-                                                                               false);
-                    const uint32_t ownr = odd ? r_hi : r_lo;
-                    w = sr_pair_into(w, k & 3, lo, hi, odd ? nbr : ownr, odd ? ownr : nbr, scale);
-                } else {
-                    switch (k & 3) {
-                    case 0: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 0); break;
-                    case 1: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 1); break;
-                    case 2: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 2); break;
-                    default: w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, lo, hi, scale, 3); break;
-                    }
-                }
-            }
+            // row-packed: both layouts hold the same code for an element (one block
+            // scale; under SR the element's own draw either way), so the row bytes
+            // come from the column words.  Nibble r & 7 of w0 (w1) is the code of
+            // v[r] for r < 8 (r >= 8).  Of a column pair, the even lane packs rows
+            // v[0..7] (its own column low, the neighbour's high), the odd lane rows
+            // v[8..15] (the neighbour's low, its own high): one word from the
+            // neighbour, then the two words' nibbles zipped into bytes.
+            const uint32_t send = odd ? w0 : w1;
+            const uint32_t recv = (uint32_t)__builtin_amdgcn_update_dpp((int)send, (int)send, 0xB1, 0xF, 0xF, false);
+            const uint32_t lo = odd ? recv : w0, hi = odd ? w1 : recv;
+            const uint32_t ev = (lo & 0x0F0F0F0Fu) | ((hi << 4) & 0xF0F0F0F0u);     // byte k: row 2k
+            const uint32_t od = ((lo >> 4) & 0x0F0F0F0Fu) | (hi & 0xF0F0F0F0u);     // byte k: row 2k + 1
+            uint32_t rowb[2] = {__builtin_amdgcn_perm(od, ev, 0x05010400u), __builtin_amdgcn_perm(od, ev, 0x07030602u)};
             if (!finite) rowb[0] = rowb[1] = 0;
 #pragma unroll
             for (int k = 0; k < 8; ++k) {
